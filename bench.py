@@ -1,0 +1,275 @@
+#!/usr/bin/env python3
+"""Benchmark of the UAD action-expert hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 200] [--warmup 20] [--workload pi0_b1]
+
+A "step" is one joint denoising step: the per-token time embedding, all
+transformer layers of the action expert over the whole chunk (attending to the
+cached prefix), and the masked per-token Euler update.  The timed region runs
+uniform 10-step schedules back to back with every input resident in HBM.
+Prints ONE JSON line (see the design notes for every field).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def gemm_bytes(M, N, K, out_bytes, extra=0):
+    """Algorithmic bytes of one projection launch: bf16 weights + bf16 input rows + output (+ extra)."""
+    return N * K * 2 + M * K * 2 + out_bytes + extra
+
+
+def kernel_bytes(wl, M):
+    """Algorithmic HBM bytes per launch of each kernel class for M tokens of workload wl."""
+    s = wl.shape
+    d, F, qd, kvd = s.d_model, s.d_ff, s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    nqkv = qd + 2 * kvd
+    keys = wl.prefix + wl.chunk
+    return {
+        "gemm_qkv": gemm_bytes(M, nqkv, d, M * nqkv * 2),
+        "attention": wl.batch * s.n_kv_heads * keys * s.head_dim * 2 * 2 + M * qd * 2 * 2,
+        "gemm_o": gemm_bytes(M, d, qd, M * d * 4 * 2),
+        "gemm_gateup": gemm_bytes(M, 2 * F, d, M * F * 2),
+        "gemm_down": gemm_bytes(M, d, F, M * d * 4 * 2),
+        "gemm_time_in": gemm_bytes(M, d, 2 * d, M * d * 2),
+        "gemm_time_out": gemm_bytes(M, d, d, M * d * 4),
+    }
+
+
+def kernel_flops(wl, M):
+    s = wl.shape
+    d, F, qd, kvd = s.d_model, s.d_ff, s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    keys = wl.prefix + wl.chunk
+    return {
+        "gemm_qkv": 2 * M * d * (qd + 2 * kvd),
+        "attention": 4 * wl.batch * s.n_heads * wl.chunk * keys * s.head_dim,
+        "gemm_o": 2 * M * qd * d,
+        "gemm_gateup": 2 * M * d * 2 * F,
+        "gemm_down": 2 * M * F * d,
+        "gemm_time_in": 2 * M * 2 * d * d,
+        "gemm_time_out": 2 * M * d * d,
+    }
+
+
+def step_bytes(wl):
+    """Algorithmic bytes of one joint step: all weights once + the prefix K/V of every env."""
+    import uad_workloads as W
+    s = wl.shape
+    return W.weight_param_count(s) * 2 + wl.batch * s.n_layers * wl.prefix * s.n_kv_heads * s.head_dim * 2 * 2
+
+
+def step_flops(wl):
+    import uad_workloads as W
+    s = wl.shape
+    M = wl.batch * wl.chunk
+    att = 4 * wl.batch * s.n_heads * wl.chunk * (wl.prefix + wl.chunk) * s.head_dim * s.n_layers
+    return 2 * M * W.weight_param_count(s) + att
+
+
+def cpu_baseline(wl, weights, prefix, noise, budgets, seconds):
+    """Time the oracle (as it stands) on this host for a bounded sample of joint steps."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    m = O.build_model(wl.shape, weights, [p[0] for p in prefix], [p[1] for p in prefix])
+    n, t, dt, mask = O.build_schedule(budgets)
+    x = noise.copy()
+    O.denoise_step(m, x, t[0], dt[0], mask[0])  # warm-up
+    done, t0 = 0, time.perf_counter()
+    while True:
+        x, _ = O.denoise_step(m, x, t[done % n], dt[done % n], mask[done % n])
+        done += 1
+        el = time.perf_counter() - t0
+        if el >= seconds and done >= 2:
+            break
+    return {"value": done / el, "unit": "denoise steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} joint steps of the {wl.name} workload (B={wl.batch}, H={wl.chunk}, "
+                      f"P={wl.prefix}) in {el:.1f} s, numpy fp32 BLAS on {platform.processor() or 'host'}",
+            "seconds": el}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="pi0_b1")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-aal", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the hot path is measured on one "
+                                   "MI355X and multi-GPU runs are not part of it", "n_gpus": a.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import uad_workloads as W
+    import paper_2609_37772_amd as U
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(2)
+    U.load_library()
+    wl = W.get_workload(a.workload)
+    s = wl.shape
+    B, H, P, M = wl.batch, wl.chunk, wl.prefix, wl.batch * wl.chunk
+    log(f"[bench] workload {wl.name}: L={s.n_layers} d={s.d_model} B={B} H={H} P={P}")
+    t0 = time.time()
+    weights = W.make_weights(wl)
+    prefix = [W.make_prefix(wl, b) for b in range(B)]
+    noise = np.stack([W.make_noise(wl, b) for b in range(B)])
+    budgets = W.make_budgets(wl)
+    ex = U.ActionExpert(s, B, H, P)
+    ex.load_weights(weights)
+    dt_ = np.uint16 if wl.bf16 else np.float32
+    K = np.empty((s.n_layers, B, P, s.n_kv_heads, s.head_dim), dt_)
+    V = np.empty_like(K)
+    for b in range(B):
+        K[:, b] = W.bf16_bits(prefix[b][0]) if wl.bf16 else prefix[b][0]
+        V[:, b] = W.bf16_bits(prefix[b][1]) if wl.bf16 else prefix[b][1]
+    ex.set_prefix_kv(K, V, B, P)
+    del K, V
+    log(f"[bench] set-up {time.time() - t0:.1f} s")
+
+    n, tg, dtg, mg = ex.schedule_tables(budgets)
+    x0 = torch.from_numpy(noise).cuda()
+    x = torch.empty_like(x0)
+
+    def run(n_sched):
+        for _ in range(n_sched):
+            x.copy_(x0)
+            ex.schedule(x, tg, dtg, mg)
+
+    n_warm = max(1, -(-a.warmup // n))
+    n_timed = max(1, -(-a.steps // n))
+    steps = n_timed * n
+    run(n_warm)
+    torch.cuda.synchronize()
+    log(f"[bench] warm-up {n_warm * n} steps done")
+    t0 = time.perf_counter()
+    run(n_timed)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    sps = steps / el
+    ms_step = 1e3 * el / steps
+    log(f"[bench] timed {steps} steps: {ms_step:.4f} ms/step, {sps:.1f} steps/s")
+
+    # Per-kernel durations: the same schedules again with HIP events around every launch
+    # (recorded by the library on the stream its kernels run on).
+    U.uad_profile_enable(ex.ctx, True)
+    run(n_timed)
+    prof = U.uad_profile_read(ex.ctx)
+    U.uad_profile_enable(ex.ctx, False)
+    kb, kf = kernel_bytes(wl, M), kernel_flops(wl, M)
+    per_kernel = {}
+    for name, (ms, cnt) in prof.items():
+        if cnt == 0:
+            continue
+        avg_us = 1e3 * ms / cnt
+        ent = {"avg_us": round(avg_us, 3), "launches": cnt, "share": None}
+        if name in kb:
+            ent["gbs"] = round(kb[name] / (avg_us * 1e-6) / 1e9, 1)
+            ent["tflops"] = round(kf[name] / (avg_us * 1e-6) / 1e12, 2)
+        per_kernel[name] = ent
+    tot = sum(v[0] for v in prof.values()) or 1.0
+    for name in per_kernel:
+        per_kernel[name]["share"] = round(prof[name][0] / tot, 4)
+    dom = max((k for k in per_kernel if k in kb), key=lambda k: prof[k][0])
+    dom_us = per_kernel[dom]["avg_us"]
+    batched = M > 400
+    if batched:
+        ach = kf[dom] / (dom_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4), "traffic": None}
+    else:
+        ach = kb[dom] / (dom_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+    roof.update({"kernel": dom, "algorithmic_bytes_per_launch": kb[dom], "avg_launch_us": dom_us})
+    sb = step_bytes(wl)
+    step_roof = {"bytes_per_step": sb, "achieved_gbs": round(sb / (ms_step * 1e-3) / 1e9, 1),
+                 "hbm_frac": round(sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "flops_per_step": step_flops(wl),
+                 "mfma_frac": round(step_flops(wl) / (ms_step * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)}
+    log(f"[bench] dominant kernel {dom}: {dom_us:.2f} us/launch, {roof['achieved']} {roof['unit']}")
+
+    out = {
+        "metric": "denoise steps/sec + action-availability latency (ms) at B=1; % HBM/MFMA roofline",
+        "value": round(sps, 2), "unit": "denoise steps/s", "n_gpus": 1, "steps": steps, "warmup": n_warm * n,
+        "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded random-init weights, N(0,1) prefix K/V and noise)",
+        "config": {"workload": wl.name, "batch": B, "chunk": H, "prefix": P, "layers": s.n_layers,
+                   "width": s.d_model, "heads": f"{s.n_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.d_ff,
+                   "action_dim": s.action_dim, "schedule": f"{wl.budget_kind} {n} steps"},
+        "roofline": roof, "step_roofline": step_roof, "kernels": per_kernel,
+    }
+
+    if not a.no_aal and B == 1:
+        out["availability"] = availability(ex, wl, noise, U, np, torch)
+
+    if not a.no_cpu_baseline:
+        log("[bench] timing the oracle on the host cores")
+        out["cpu_baseline"] = cpu_baseline(wl, weights, prefix, noise, budgets, a.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    ex.close()
+
+
+def availability(ex, wl, noise, U, np, torch, reps=20):
+    """Release times of the S executed actions and AAL (App. B / App. D.3) for the
+    vanilla uniform schedule and the UAD 4/7/10 schedule on this model."""
+    import uad_workloads as W
+    hz = ex.tick_rate_hz()
+    S = wl.executed
+    res = {}
+    sched = {"vanilla_uniform_10": np.full((1, wl.chunk), 10, np.int32),
+             "uad_4_7_10": W.make_budgets(W.get_workload("pi0_b1_uad"))}
+    for name, bud in sched.items():
+        n, tg, dtg, mg = ex.schedule_tables(bud)
+        x0 = torch.from_numpy(noise).cuda()
+        x = torch.empty_like(x0)
+        ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
+        rst = torch.zeros((1, wl.chunk), dtype=torch.int32, device="cuda")
+        step_ms = []
+        for r in range(reps + 2):
+            x.copy_(x0)
+            ex.schedule(x, tg, dtg, mg, None, rst, ticks)
+            torch.cuda.synchronize()
+            tk = ticks.numpy().astype(np.int64)
+            if r >= 2:
+                step_ms.append((tk[1:] - tk[0]) / hz * 1e3)
+        step_ms = np.median(np.stack(step_ms), axis=0)  # time at the end of each step
+        rs = rst.cpu().numpy()[0, :S]
+        rel = [float(step_ms[k]) for k in rs]
+        ent = {"release_ms_executed": [round(v, 4) for v in rel], "ttfr_ms": round(min(rel), 4)}
+        for tact in (50.0, 12.5):
+            ent[f"aal_ms_tact_{tact:g}"] = round(U.uad_aal(rel, tact), 5)
+        res[name] = ent
+    v, u = res["vanilla_uniform_10"], res["uad_4_7_10"]
+    res["aal_speedup_tact_12.5"] = round(v["aal_ms_tact_12.5"] / u["aal_ms_tact_12.5"], 3)
+    return res
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,207 @@
+/*
+ * uad.h - C ABI of the Urgency-Aware Denoising (UAD) action-expert library
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The library evaluates the flow-matching action expert F_theta jointly over
+ * an action chunk whose tokens each carry their own flow time, attends every
+ * chunk token to a cached vision-language prefix K/V and to the chunk, and
+ * applies the per-token Euler update that freezes released urgent actions
+ * while tail actions keep refining (Sec. 3 Eqs. 1-2; Sec. 4.2 Eqs. 3-5;
+ * App. C.1 "Per-Action Time Conditioning").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every call returns a uad_status; nothing aborts or prints.  On a non-OK
+ *    status uad_last_error(ctx) holds a message naming the offending argument
+ *    or tensor.  Validation happens before any device work is enqueued.
+ *  - Device work is enqueued asynchronously on the context's HIP stream.
+ *    Caller-owned device buffers (x, t, dt, masks, outputs) are borrowed
+ *    only for the duration of that enqueued work; keep them alive until
+ *    uad_synchronize() or an equivalent synchronisation of that stream.
+ *  - Token order: token m = b * chunk + i for environment b and action i.
+ *    Flow time runs from t = 1 (noise) to t = 0; the Euler step is
+ *    x <- x + dt * v with dt = -1/N_i for an action with budget N_i.
+ *  - A context is not thread-safe; use one per host thread.
+ *  - Weights are named tensors in PyTorch Linear layout [out][in], row-major:
+ *      action_in.w [d][Da], action_in.b [d],
+ *      time_mlp_in.w [d][2d], time_mlp_in.b [d],
+ *      time_mlp_out.w [d][d], time_mlp_out.b [d],
+ *      layers.<l>.attn_norm [d], layers.<l>.wq [Hq*hd][d],
+ *      layers.<l>.wk [Hkv*hd][d], layers.<l>.wv [Hkv*hd][d],
+ *      layers.<l>.wo [d][Hq*hd], layers.<l>.mlp_norm [d],
+ *      layers.<l>.w_gate [F][d], layers.<l>.w_up [F][d], layers.<l>.w_down [d][F],
+ *      final_norm [d], action_out.w [Da][d], action_out.b [Da].
+ *    The action expert is a pre-norm transformer: per-token time embedding
+ *    e_j = sin(w_j t), e_{j+d/2} = cos(w_j t), w_j = 1000 * 10000^(-j/(d/2)),
+ *    concatenated to the projected action and passed through a SiLU MLP; then
+ *    per layer RMSNorm -> Q/K/V -> attention over [prefix ; chunk] (no mask,
+ *    query head j uses KV head floor(j*Hkv/Hq), scale 1/sqrt(hd)) -> output
+ *    projection + residual -> RMSNorm -> GeGLU (tanh GELU) MLP + residual;
+ *    final RMSNorm and action projection give the velocity.
+ */
+#ifndef UAD_H
+#define UAD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct uad_ctx uad_ctx; /* opaque, owned by the library */
+
+typedef enum {
+  UAD_OK = 0,
+  UAD_E_INVALID = 1,     /* null pointer, non-positive size, bad dtype/flag */
+  UAD_E_SHAPE = 2,       /* size beyond the context's maxima, tensor shape mismatch */
+  UAD_E_STATE = 3,       /* weights or prefix not loaded yet */
+  UAD_E_MISSING = 4,     /* a required weight tensor is absent or duplicated */
+  UAD_E_HIP = 5,         /* a HIP runtime call failed (message has hipGetErrorString) */
+  UAD_E_OOM = 6,         /* device allocation failed */
+  UAD_E_UNSUPPORTED = 7  /* model dimensions the kernels do not support */
+} uad_status;
+
+enum { UAD_DTYPE_F32 = 0, UAD_DTYPE_BF16 = 1 };
+
+typedef struct {
+  int32_t n_layers;   /* L */
+  int32_t d_model;    /* d, multiple of 32 */
+  int32_t n_heads;    /* Hq */
+  int32_t n_kv_heads; /* Hkv, divides Hq */
+  int32_t head_dim;   /* hd in {64, 128, 256} */
+  int32_t d_ff;       /* F, multiple of 32 */
+  int32_t action_dim; /* Da, 1..64 */
+  int32_t max_batch;  /* largest batch B of any later call */
+  int32_t max_chunk;  /* largest chunk H of any later call */
+  int32_t max_prefix; /* largest prefix length P */
+  float rms_eps;      /* RMSNorm epsilon (1e-6 in the bundled workloads) */
+  int32_t flags;      /* reserved, must be 0 */
+} uad_model_config;
+
+typedef struct {
+  const char *name;  /* one of the names listed above */
+  const void *data;  /* host or device pointer, row-major, dense */
+  int32_t dtype;     /* UAD_DTYPE_F32 or UAD_DTYPE_BF16 */
+  int32_t ndim;      /* 1 or 2 */
+  int64_t shape[4];
+  int32_t on_device; /* 1 if data is a device pointer */
+} uad_tensor;
+
+/* Create a context on HIP device `device`.  `hip_stream` is a hipStream_t on
+ * that device, or NULL to let the library create its own.  Allocates the
+ * weight store, the prefix/chunk K/V store and all activation workspace for
+ * the configured maxima.  Errors: UAD_E_INVALID (null/negative fields),
+ * UAD_E_UNSUPPORTED (dimension the kernels cannot tile), UAD_E_OOM, UAD_E_HIP.
+ * On error *out is set to NULL. */
+uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_stream, uad_ctx **out);
+
+/* Free every device buffer of the context (after synchronising its stream). */
+void uad_destroy(uad_ctx *ctx);
+
+/* Message for the last non-OK status returned for this context (empty if none).
+ * With ctx == NULL: the message of the last failed uad_create on this thread. */
+const char *uad_last_error(const uad_ctx *ctx);
+
+/* Re-target the context at another stream of the same device (NULL: own). */
+uad_status uad_set_stream(uad_ctx *ctx, void *hip_stream);
+
+/* Load the action-expert parameters theta of F_theta (Sec. 3 Eq. 1).
+ * `tensors` must name every weight listed at the top exactly once, with the
+ * listed shape; dtype F32 or BF16 (F32 values are rounded to bf16,
+ * nearest-even, for the large projections; norm gains, biases and the
+ * action in/out projections are kept in fp32).  The data are COPIED into
+ * library-owned device memory in the kernels' packed layout; the caller may
+ * free its buffers on return.  Synchronous.  Errors: UAD_E_MISSING (absent or
+ * duplicated name, named in the message), UAD_E_SHAPE, UAD_E_INVALID, UAD_E_HIP. */
+uad_status uad_load_weights(uad_ctx *ctx, const uad_tensor *tensors, int32_t n_tensors);
+
+/* Set the cached context of the action expert: the per-layer key/value
+ * vectors of the P vision-language prefix tokens (the o, L conditioning of
+ * Sec. 3 Eq. 1), for `batch` environments.  k and v are dense
+ * [L][batch][P][Hkv][hd] arrays of `dtype` (F32 rounded to bf16, nearest-even),
+ * host memory (on_device = 0) or device memory (on_device = 1).  COPIED into
+ * the library's K/V store, where each step appends the chunk's own keys and
+ * values after the prefix.  Synchronous.  Errors: UAD_E_INVALID,
+ * UAD_E_SHAPE (batch > max_batch, P > max_prefix), UAD_E_HIP. */
+uad_status uad_set_prefix_kv(uad_ctx *ctx, const void *k, const void *v, int32_t dtype,
+                             int32_t batch, int32_t prefix_len, int32_t on_device);
+
+/* One denoising step (Sec. 3 Eq. 1 with per-token time, App. C.1; Sec. 4.2
+ * Eq. 5): ONE joint evaluation v = F_theta(x, t) over all batch*chunk tokens
+ * -- frozen tokens included, they remain keys/values of the others -- then the
+ * per-token Euler update x_i <- x_i + dt_i * v_i for tokens with
+ * mask_i == 0 and dt_i != 0; other tokens are copied unchanged (bit-identical).
+ *   x      device fp32 [batch][chunk][Da], in/out
+ *   t, dt  device fp32 [batch][chunk]
+ *   mask   device uint8 [batch][chunk], 1 = released/frozen
+ *   v_out  device fp32 [batch][chunk][Da] or NULL: receives the velocity
+ * Environment b attends to prefix environment b.  Requires weights and a
+ * prefix set for >= batch environments (else UAD_E_STATE).  Errors:
+ * UAD_E_INVALID (null pointer, batch/chunk < 1), UAD_E_SHAPE (beyond maxima),
+ * UAD_E_STATE, UAD_E_HIP. */
+uad_status uad_denoise_step(uad_ctx *ctx, float *x, const float *t, const float *dt,
+                            const uint8_t *mask, float *v_out, int32_t batch, int32_t chunk);
+
+/* A whole per-token schedule (Sec. 4.2 Eqs. 4-5): n_steps joint steps, step k
+ * using the k-th slice of the tables.
+ *   x                     device fp32 [batch][chunk][Da], in/out (x_0 in, final out)
+ *   t_sched, dt_sched     device fp32 [n_steps][batch][chunk]
+ *   mask_sched            device uint8 [n_steps][batch][chunk]
+ *   released              device fp32 [batch][chunk][Da] or NULL: a^i = x^i right
+ *                         after token i's release step
+ *   release_step          device int32 [batch][chunk] or NULL: that step (0-based),
+ *                         left untouched for a token that is never active
+ *   step_ticks            pinned host uint64 [n_steps + 1] or NULL: device
+ *                         wall-clock ticks at the schedule start and after each
+ *                         step (see uad_tick_rate_hz)
+ * A token's release step is the last step at which it is updated: the step k
+ * with mask==0 and dt!=0 whose next step has mask==1, or the final step.
+ * Errors as uad_denoise_step. */
+uad_status uad_denoise_schedule(uad_ctx *ctx, float *x, const float *t_sched, const float *dt_sched,
+                                const uint8_t *mask_sched, int32_t n_steps, int32_t batch, int32_t chunk,
+                                float *released, int32_t *release_step, uint64_t *step_ticks);
+
+/* Build the per-step tables from integer budgets N_i (Sec. 4.2 Eq. 4): pure
+ * host code, no context needed.  budgets: host int32 [batch][chunk], each in
+ * 1..max_steps.  Outputs (host, caller-allocated, capacity max_steps slices):
+ * *n_steps = max N_i; t[k] = (N_i - min(k, N_i)) / N_i (fp32 division of
+ * integers); dt[k] = -(1/N_i) while k < N_i, else 0; mask[k] = (k >= N_i).
+ * Errors: UAD_E_INVALID (null pointer, size < 1, a budget outside 1..max_steps). */
+uad_status uad_build_schedule(const int32_t *budgets, int32_t batch, int32_t chunk, int32_t max_steps,
+                              int32_t *n_steps, float *t, float *dt, uint8_t *mask);
+
+/* Average action-availability latency of a controller that executes actions in
+ * order, each for t_act, starting each action as soon as it is released and
+ * the previous one finished (App. B timing model, App. D.3 measurement):
+ * AAL = (sum of waits) / n.  release[j] is the release time of executed
+ * action j measured from the request.  Pure host code. */
+uad_status uad_aal(const double *release, int32_t n, double t_act, double *aal_out);
+
+/* Block the host until all work enqueued on the context's stream is done. */
+uad_status uad_synchronize(uad_ctx *ctx);
+
+/* Device wall-clock tick rate (Hz) of the counter written to step_ticks. */
+uad_status uad_tick_rate_hz(uad_ctx *ctx, double *hz);
+
+/* Test hook: when enabled, steps skip F_theta and use the synthetic velocity
+ * field v = alpha * x + beta, so the integrator and schedule can be checked
+ * against the closed-form Euler solution. */
+uad_status uad_debug_velocity_field(uad_ctx *ctx, int32_t enable, float alpha, float beta);
+
+/* Measurement hook: while enabled, every kernel launch of a step is bracketed
+ * by a pair of HIP events recorded on the context's stream, grouped by kernel
+ * class.  Enabling resets the totals. */
+uad_status uad_profile_enable(uad_ctx *ctx, int32_t enable);
+
+/* Read the totals of kernel class `index` (0-based; UAD_E_INVALID past the
+ * last class): its name (NUL-terminated, truncated to name_cap), the summed
+ * event-measured duration in milliseconds and the number of launches.
+ * Synchronises the context's stream first. */
+uad_status uad_profile_read(uad_ctx *ctx, int32_t index, char *name, int32_t name_cap, double *total_ms,
+                            int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UAD_H */

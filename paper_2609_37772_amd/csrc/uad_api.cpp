@@ -1,0 +1,689 @@
+// C ABI of libuad: context management, argument validation, weight and
+// prefix repacking into the kernels' device layouts, and the launch sequence
+// of one joint denoising step.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "uad_internal.h"
+
+using namespace uad;
+
+namespace {
+
+thread_local std::string g_create_err;
+
+uad_status fail(uad_ctx *c, uad_status st, const std::string &msg) {
+  if (c) c->err = msg;
+  return st;
+}
+
+uad_status hip_fail(uad_ctx *c, hipError_t e, const char *what) {
+  return fail(c, UAD_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x7FFFFFu)) return (uint16_t)((u >> 16) | 0x40);  // quiet NaN
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+float bf16_to_f32(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+// Copy a caller tensor (host or device, f32 or bf16) to a host fp32 vector.
+bool fetch_f32(const void *data, int dtype, int on_device, size_t n, std::vector<float> *out, std::string *err) {
+  out->resize(n);
+  const size_t esz = dtype == UAD_DTYPE_F32 ? 4 : 2;
+  std::vector<uint8_t> tmp;
+  const void *src = data;
+  if (on_device) {
+    tmp.resize(n * esz);
+    hipError_t e = hipMemcpy(tmp.data(), data, n * esz, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+      *err = std::string("hipMemcpy(D2H): ") + hipGetErrorString(e);
+      return false;
+    }
+    src = tmp.data();
+  }
+  if (dtype == UAD_DTYPE_F32) {
+    std::memcpy(out->data(), src, n * 4);
+  } else {
+    const uint16_t *s = (const uint16_t *)src;
+    for (size_t i = 0; i < n; ++i) (*out)[i] = bf16_to_f32(s[i]);
+  }
+  return true;
+}
+
+// Pack row-major W[N][K] into the MFMA fragment order (see uad_internal.h),
+// writing 16-row tile nt to destination tile (tile_base + nt * tile_step).
+void pack_tiles(const float *W, int N, int K, uint16_t *dst, int tile_base, int tile_step) {
+  const int KB = K / kTileK;
+  for (int nt = 0; nt < N / kTileN; ++nt) {
+    uint16_t *tb = dst + (size_t)(tile_base + nt * tile_step) * KB * kBlockElems;
+    for (int kb = 0; kb < KB; ++kb)
+      for (int l = 0; l < 64; ++l)
+        for (int e = 0; e < 8; ++e)
+          tb[((size_t)kb * 64 + l) * 8 + e] =
+              f32_to_bf16_rne(W[(size_t)(nt * kTileN + (l & 15)) * K + kb * kTileK + (l >> 4) * 8 + e]);
+  }
+}
+
+struct Carve {
+  size_t off = 0;
+  template <class T>
+  size_t take(size_t n) {
+    size_t o = off;
+    off = align256(off + n * sizeof(T));
+    return o;
+  }
+};
+
+// Kernel classes reported by the measurement hook.
+enum KClass { K_TEMB, K_GEMM_TIME_IN, K_GEMM_TIME_OUT, K_RMSNORM, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP,
+              K_GEMM_DOWN, K_FINAL, K_NCLASS };
+const char *kClassNames[K_NCLASS] = {"temb", "gemm_time_in", "gemm_time_out", "rmsnorm", "gemm_qkv", "attention",
+                                     "gemm_o", "gemm_gateup", "gemm_down", "final_euler"};
+
+hipEvent_t pool_event(uad_ctx *c) {
+  if (!c->ev_pool.empty()) {
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+
+int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) {
+  const int rows = (c->Hq / c->Hkv) * H;
+  const int qblocks = (rows + 63) / 64;
+  const int n_blocks = (P + H + 31) / 32;
+  const int wgs = qblocks * B * c->Hkv;
+  int want = (256 + wgs - 1) / wgs;
+  int maxs = n_blocks / 4;
+  if (maxs < 1) maxs = 1;
+  if (want > maxs) want = maxs;
+  if (want < 1) want = 1;
+  const int per = (n_blocks + want - 1) / want;
+  *bps = per;
+  return (n_blocks + per - 1) / per;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *uad_last_error(const uad_ctx *ctx) { return ctx ? ctx->err.c_str() : g_create_err.c_str(); }
+
+uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_stream, uad_ctx **out) {
+  if (out) *out = nullptr;
+  auto cerr = [](uad_status st, const std::string &m) {
+    g_create_err = m;
+    return st;
+  };
+  if (!cfg || !out) return cerr(UAD_E_INVALID, "uad_create: null cfg/out");
+  const uad_model_config &m = *cfg;
+  if (m.n_layers < 1 || m.d_model < 1 || m.n_heads < 1 || m.n_kv_heads < 1 || m.head_dim < 1 || m.d_ff < 1 ||
+      m.action_dim < 1 || m.max_batch < 1 || m.max_chunk < 1 || m.max_prefix < 0 || !(m.rms_eps >= 0.f))
+    return cerr(UAD_E_INVALID, "uad_create: every dimension must be positive");
+  if (m.flags != 0) return cerr(UAD_E_INVALID, "uad_create: flags must be 0");
+  if (m.d_model % 32 || m.d_ff % 32) return cerr(UAD_E_UNSUPPORTED, "uad_create: d_model and d_ff must be multiples of 32");
+  if (m.head_dim != 64 && m.head_dim != 128 && m.head_dim != 256)
+    return cerr(UAD_E_UNSUPPORTED, "uad_create: head_dim must be 64, 128 or 256");
+  if (m.n_heads % m.n_kv_heads) return cerr(UAD_E_UNSUPPORTED, "uad_create: n_kv_heads must divide n_heads");
+  if (m.action_dim > 64) return cerr(UAD_E_UNSUPPORTED, "uad_create: action_dim must be <= 64");
+
+  hipError_t e = hipSetDevice(device);
+  if (e != hipSuccess) return cerr(UAD_E_HIP, std::string("hipSetDevice: ") + hipGetErrorString(e));
+
+  uad_ctx *c = new uad_ctx();
+  c->cfg = m;
+  c->device = device;
+  c->d = m.d_model;
+  c->L = m.n_layers;
+  c->Hq = m.n_heads;
+  c->Hkv = m.n_kv_heads;
+  c->hd = m.head_dim;
+  c->F = m.d_ff;
+  c->Da = m.action_dim;
+  c->q_dim = c->Hq * c->hd;
+  c->kv_dim = c->Hkv * c->hd;
+  c->n_qkv = c->q_dim + 2 * c->kv_dim;
+  c->m_alloc = round_up(m.max_batch * m.max_chunk, 64);
+  c->s_alloc = round_up(m.max_prefix + m.max_chunk, 32);
+  c->layers.resize(c->L);
+
+  if (hip_stream) {
+    c->stream = (hipStream_t)hip_stream;
+  } else {
+    e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      delete c;
+      return cerr(UAD_E_HIP, std::string("hipStreamCreate: ") + hipGetErrorString(e));
+    }
+    c->own_stream = true;
+  }
+  int rate_khz = 0;
+  if (hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, device) == hipSuccess && rate_khz > 0)
+    c->tick_hz = rate_khz * 1000.0;
+  else
+    c->tick_hz = 1e8;
+
+  // weight store
+  const int d = c->d, F = c->F, Da = c->Da;
+  Carve w;
+  size_t o_ain = w.take<float>((size_t)d * Da), o_ainb = w.take<float>(d), o_t1b = w.take<float>(d),
+         o_t2b = w.take<float>(d), o_fn = w.take<float>(d), o_aout = w.take<float>((size_t)Da * d),
+         o_aoutb = w.take<float>(Da), o_freq = w.take<float>(d / 2), o_t1 = w.take<uint16_t>((size_t)d * 2 * d),
+         o_t2 = w.take<uint16_t>((size_t)d * d);
+  std::vector<size_t> o_l(6 * c->L);
+  for (int l = 0; l < c->L; ++l) {
+    o_l[6 * l + 0] = w.take<uint16_t>((size_t)c->n_qkv * d);
+    o_l[6 * l + 1] = w.take<uint16_t>((size_t)d * c->q_dim);
+    o_l[6 * l + 2] = w.take<uint16_t>((size_t)2 * F * d);
+    o_l[6 * l + 3] = w.take<uint16_t>((size_t)d * F);
+    o_l[6 * l + 4] = w.take<float>(d);
+    o_l[6 * l + 5] = w.take<float>(d);
+  }
+  c->wbytes = w.off;
+  e = hipMalloc(&c->wbuf, c->wbytes);
+  if (e != hipSuccess) {
+    uad_destroy(c);
+    return cerr(UAD_E_OOM, std::string("hipMalloc(weights): ") + hipGetErrorString(e));
+  }
+  char *wb = (char *)c->wbuf;
+  c->action_in_w = (float *)(wb + o_ain);
+  c->action_in_b = (float *)(wb + o_ainb);
+  c->t1_b = (float *)(wb + o_t1b);
+  c->t2_b = (float *)(wb + o_t2b);
+  c->final_norm = (float *)(wb + o_fn);
+  c->action_out_w = (float *)(wb + o_aout);
+  c->action_out_b = (float *)(wb + o_aoutb);
+  c->freqs = (float *)(wb + o_freq);
+  c->t1_w = (__bf16 *)(wb + o_t1);
+  c->t2_w = (__bf16 *)(wb + o_t2);
+  for (int l = 0; l < c->L; ++l) {
+    c->layers[l].wqkv = (const __bf16 *)(wb + o_l[6 * l + 0]);
+    c->layers[l].wo = (const __bf16 *)(wb + o_l[6 * l + 1]);
+    c->layers[l].wgu = (const __bf16 *)(wb + o_l[6 * l + 2]);
+    c->layers[l].wdown = (const __bf16 *)(wb + o_l[6 * l + 3]);
+    c->layers[l].attn_norm = (const float *)(wb + o_l[6 * l + 4]);
+    c->layers[l].mlp_norm = (const float *)(wb + o_l[6 * l + 5]);
+  }
+  // time-embedding frequencies w_j = 1000 * 10000^(-j/(d/2)), computed in double
+  {
+    std::vector<float> fr(d / 2);
+    for (int j = 0; j < d / 2; ++j) fr[j] = (float)(1000.0 * std::pow(10000.0, -(double)j / (double)(d / 2)));
+    e = hipMemcpy(c->freqs, fr.data(), fr.size() * 4, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      uad_destroy(c);
+      return cerr(UAD_E_HIP, std::string("hipMemcpy(freqs): ") + hipGetErrorString(e));
+    }
+  }
+
+  // K / V^T store: [L][max_batch][Hkv][s_alloc][hd] and [L][max_batch][Hkv][hd][s_alloc]
+  c->kv_layer_elems = (size_t)m.max_batch * c->Hkv * c->s_alloc * c->hd;
+  const size_t kv_bytes = c->kv_layer_elems * c->L * 2;
+  e = hipMalloc((void **)&c->kcache, kv_bytes);
+  if (e == hipSuccess) e = hipMalloc((void **)&c->vtcache, kv_bytes);
+  if (e == hipSuccess) e = hipMemset(c->kcache, 0, kv_bytes);
+  if (e == hipSuccess) e = hipMemset(c->vtcache, 0, kv_bytes);
+  if (e != hipSuccess) {
+    uad_destroy(c);
+    return cerr(UAD_E_OOM, std::string("hipMalloc(kv store): ") + hipGetErrorString(e));
+  }
+
+  // activation workspace (rows padded to 64 and zeroed so padded rows stay finite)
+  size_t part = 0;
+  for (int B = 1; B <= m.max_batch; ++B)
+    for (int H = 1; H <= m.max_chunk; ++H) {
+      int bps;
+      const int sp = attn_splits(c, B, H, m.max_prefix, &bps);
+      if (sp > 1) {
+        const size_t rows_pad = (size_t)((c->Hq / c->Hkv) * H + 63) / 64 * 64;
+        part = std::max(part, (size_t)sp * B * c->Hkv * rows_pad);
+      }
+    }
+  c->attn_part_elems = part;
+  const size_t M = c->m_alloc;
+  Carve a;
+  // GEMM inputs (te, z, n, o, g) hold two bf16 planes (hi, lo) of M rows each
+  size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(2 * M * 2 * d), o_z = a.take<uint16_t>(2 * M * d),
+         o_n = a.take<uint16_t>(2 * M * d), o_o = a.take<uint16_t>(2 * M * c->q_dim), o_g = a.take<uint16_t>(2 * M * F),
+         o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
+         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2);
+  e = hipMalloc(&c->abuf, a.off);
+  if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
+  if (e != hipSuccess) {
+    uad_destroy(c);
+    return cerr(UAD_E_OOM, std::string("hipMalloc(workspace): ") + hipGetErrorString(e));
+  }
+  char *ab = (char *)c->abuf;
+  c->h = (float *)(ab + o_h);
+  c->a_te = (__bf16 *)(ab + o_te);
+  c->a_z = (__bf16 *)(ab + o_z);
+  c->a_n = (__bf16 *)(ab + o_n);
+  c->a_o = (__bf16 *)(ab + o_o);
+  c->a_g = (__bf16 *)(ab + o_g);
+  c->q = (__bf16 *)(ab + o_q);
+  c->attn_opart = (float *)(ab + o_op);
+  c->attn_ml = (float *)(ab + o_ml);
+  *out = c;
+  g_create_err.clear();
+  return UAD_OK;
+}
+
+void uad_destroy(uad_ctx *c) {
+  if (!c) return;
+  (void)hipSetDevice(c->device);
+  if (c->stream) (void)hipStreamSynchronize(c->stream);
+  if (c->wbuf) (void)hipFree(c->wbuf);
+  if (c->kcache) (void)hipFree(c->kcache);
+  if (c->vtcache) (void)hipFree(c->vtcache);
+  if (c->abuf) (void)hipFree(c->abuf);
+  for (auto &r : c->prof_pending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
+  if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
+  delete c;
+}
+
+uad_status uad_set_stream(uad_ctx *c, void *hip_stream) {
+  if (!c) return UAD_E_INVALID;
+  (void)hipSetDevice(c->device);
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+  if (hip_stream) {
+    if (c->own_stream) (void)hipStreamDestroy(c->stream);
+    c->own_stream = false;
+    c->stream = (hipStream_t)hip_stream;
+  } else if (!c->own_stream) {
+    e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return hip_fail(c, e, "hipStreamCreate");
+    c->own_stream = true;
+  }
+  return UAD_OK;
+}
+
+uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
+  if (!c) return UAD_E_INVALID;
+  if (!ts || n < 1) return fail(c, UAD_E_INVALID, "uad_load_weights: no tensors");
+  (void)hipSetDevice(c->device);
+  const int d = c->d, F = c->F, Da = c->Da;
+  // required names and shapes
+  std::map<std::string, std::vector<int64_t>> need;
+  need["action_in.w"] = {d, Da};
+  need["action_in.b"] = {d};
+  need["time_mlp_in.w"] = {d, 2 * d};
+  need["time_mlp_in.b"] = {d};
+  need["time_mlp_out.w"] = {d, d};
+  need["time_mlp_out.b"] = {d};
+  need["final_norm"] = {d};
+  need["action_out.w"] = {Da, d};
+  need["action_out.b"] = {Da};
+  for (int l = 0; l < c->L; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    need[p + "attn_norm"] = {d};
+    need[p + "wq"] = {c->q_dim, d};
+    need[p + "wk"] = {c->kv_dim, d};
+    need[p + "wv"] = {c->kv_dim, d};
+    need[p + "wo"] = {d, c->q_dim};
+    need[p + "mlp_norm"] = {d};
+    need[p + "w_gate"] = {F, d};
+    need[p + "w_up"] = {F, d};
+    need[p + "w_down"] = {d, F};
+  }
+  std::map<std::string, const uad_tensor *> got;
+  for (int i = 0; i < n; ++i) {
+    const uad_tensor &t = ts[i];
+    if (!t.name || !t.data) return fail(c, UAD_E_INVALID, "uad_load_weights: tensor with null name or data");
+    auto it = need.find(t.name);
+    if (it == need.end()) return fail(c, UAD_E_MISSING, std::string("uad_load_weights: unknown tensor ") + t.name);
+    if (got.count(t.name)) return fail(c, UAD_E_MISSING, std::string("uad_load_weights: duplicated tensor ") + t.name);
+    if (t.dtype != UAD_DTYPE_F32 && t.dtype != UAD_DTYPE_BF16)
+      return fail(c, UAD_E_INVALID, std::string("uad_load_weights: bad dtype for ") + t.name);
+    const auto &shp = it->second;
+    bool ok = t.ndim == (int)shp.size();
+    for (size_t k = 0; ok && k < shp.size(); ++k) ok = t.shape[k] == shp[k];
+    if (!ok) return fail(c, UAD_E_SHAPE, std::string("uad_load_weights: wrong shape for ") + t.name);
+    got[t.name] = &t;
+  }
+  for (auto &kv : need)
+    if (!got.count(kv.first)) return fail(c, UAD_E_MISSING, "uad_load_weights: missing tensor " + kv.first);
+
+  std::string err;
+  auto host = [&](const std::string &name, std::vector<float> *v) {
+    const uad_tensor *t = got[name];
+    size_t cnt = 1;
+    for (int k = 0; k < t->ndim; ++k) cnt *= (size_t)t->shape[k];
+    return fetch_f32(t->data, t->dtype, t->on_device, cnt, v, &err);
+  };
+  auto up = [&](void *dst, const void *src, size_t bytes) {
+    hipError_t e = hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) err = std::string("hipMemcpy(H2D): ") + hipGetErrorString(e);
+    return e == hipSuccess;
+  };
+  std::vector<float> v1, v2, v3;
+  std::vector<uint16_t> pk;
+  auto put_f32 = [&](const std::string &name, float *dst) {
+    return host(name, &v1) && up(dst, v1.data(), v1.size() * 4);
+  };
+  bool ok = put_f32("action_in.w", c->action_in_w) && put_f32("action_in.b", c->action_in_b) &&
+            put_f32("time_mlp_in.b", c->t1_b) && put_f32("time_mlp_out.b", c->t2_b) &&
+            put_f32("final_norm", c->final_norm) && put_f32("action_out.w", c->action_out_w) &&
+            put_f32("action_out.b", c->action_out_b);
+  if (ok && (ok = host("time_mlp_in.w", &v1))) {
+    pk.assign((size_t)d * 2 * d, 0);
+    pack_tiles(v1.data(), d, 2 * d, pk.data(), 0, 1);
+    ok = up(c->t1_w, pk.data(), pk.size() * 2);
+  }
+  if (ok && (ok = host("time_mlp_out.w", &v1))) {
+    pk.assign((size_t)d * d, 0);
+    pack_tiles(v1.data(), d, d, pk.data(), 0, 1);
+    ok = up(c->t2_w, pk.data(), pk.size() * 2);
+  }
+  for (int l = 0; ok && l < c->L; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    uad_layer_ptrs &lp = c->layers[l];
+    ok = put_f32(p + "attn_norm", (float *)lp.attn_norm) && put_f32(p + "mlp_norm", (float *)lp.mlp_norm);
+    if (!ok) break;
+    // fused QKV: tiles [q | k | v]
+    pk.assign((size_t)c->n_qkv * d, 0);
+    ok = host(p + "wq", &v1) && host(p + "wk", &v2) && host(p + "wv", &v3);
+    if (!ok) break;
+    pack_tiles(v1.data(), c->q_dim, d, pk.data(), 0, 1);
+    pack_tiles(v2.data(), c->kv_dim, d, pk.data(), c->q_dim / kTileN, 1);
+    pack_tiles(v3.data(), c->kv_dim, d, pk.data(), (c->q_dim + c->kv_dim) / kTileN, 1);
+    ok = up((void *)lp.wqkv, pk.data(), pk.size() * 2);
+    if (!ok) break;
+    ok = host(p + "wo", &v1);
+    if (!ok) break;
+    pk.assign((size_t)d * c->q_dim, 0);
+    pack_tiles(v1.data(), d, c->q_dim, pk.data(), 0, 1);
+    ok = up((void *)lp.wo, pk.data(), pk.size() * 2);
+    if (!ok) break;
+    // gate/up interleaved per 16-column tile: tile 2j = gate j, tile 2j+1 = up j
+    ok = host(p + "w_gate", &v1) && host(p + "w_up", &v2);
+    if (!ok) break;
+    pk.assign((size_t)2 * F * d, 0);
+    pack_tiles(v1.data(), F, d, pk.data(), 0, 2);
+    pack_tiles(v2.data(), F, d, pk.data(), 1, 2);
+    ok = up((void *)lp.wgu, pk.data(), pk.size() * 2);
+    if (!ok) break;
+    ok = host(p + "w_down", &v1);
+    if (!ok) break;
+    pk.assign((size_t)d * F, 0);
+    pack_tiles(v1.data(), d, F, pk.data(), 0, 1);
+    ok = up((void *)lp.wdown, pk.data(), pk.size() * 2);
+  }
+  if (!ok) {
+    c->weights_loaded = false;
+    return fail(c, UAD_E_HIP, "uad_load_weights: " + err);
+  }
+  c->weights_loaded = true;
+  return UAD_OK;
+}
+
+uad_status uad_set_prefix_kv(uad_ctx *c, const void *k, const void *v, int32_t dtype, int32_t batch,
+                             int32_t prefix_len, int32_t on_device) {
+  if (!c) return UAD_E_INVALID;
+  if (!k || !v) return fail(c, UAD_E_INVALID, "uad_set_prefix_kv: null k/v");
+  if (dtype != UAD_DTYPE_F32 && dtype != UAD_DTYPE_BF16) return fail(c, UAD_E_INVALID, "uad_set_prefix_kv: bad dtype");
+  if (batch < 1 || prefix_len < 0) return fail(c, UAD_E_INVALID, "uad_set_prefix_kv: batch must be >= 1, prefix_len >= 0");
+  if (batch > c->cfg.max_batch) return fail(c, UAD_E_SHAPE, "uad_set_prefix_kv: batch > max_batch");
+  if (prefix_len > c->cfg.max_prefix) return fail(c, UAD_E_SHAPE, "uad_set_prefix_kv: prefix_len > max_prefix");
+  (void)hipSetDevice(c->device);
+  const int L = c->L, Hkv = c->Hkv, hd = c->hd, P = prefix_len, S = c->s_alloc;
+  const size_t per_layer_in = (size_t)batch * P * Hkv * hd;
+  std::string err;
+  std::vector<float> kf, vf;
+  std::vector<uint16_t> ks((size_t)batch * Hkv * S * hd), vs((size_t)batch * Hkv * hd * S);
+  const size_t esz = dtype == UAD_DTYPE_F32 ? 4 : 2;
+  for (int l = 0; l < L; ++l) {
+    if (!fetch_f32((const char *)k + l * per_layer_in * esz, dtype, on_device, per_layer_in, &kf, &err) ||
+        !fetch_f32((const char *)v + l * per_layer_in * esz, dtype, on_device, per_layer_in, &vf, &err))
+      return fail(c, UAD_E_HIP, "uad_set_prefix_kv: " + err);
+    std::fill(ks.begin(), ks.end(), 0);
+    std::fill(vs.begin(), vs.end(), 0);
+    for (int b = 0; b < batch; ++b)
+      for (int s = 0; s < P; ++s)
+        for (int g = 0; g < Hkv; ++g)
+          for (int cc = 0; cc < hd; ++cc) {
+            const size_t src = (((size_t)b * P + s) * Hkv + g) * hd + cc;
+            const size_t eh = (size_t)b * Hkv + g;
+            ks[(eh * S + s) * hd + cc] = f32_to_bf16_rne(kf[src]);
+            vs[(eh * hd + cc) * S + s] = f32_to_bf16_rne(vf[src]);
+          }
+    hipError_t e = hipMemcpy(c->kcache + l * c->kv_layer_elems, ks.data(), ks.size() * 2, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(c->vtcache + l * c->kv_layer_elems, vs.data(), vs.size() * 2, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(c, e, "uad_set_prefix_kv: hipMemcpy");
+  }
+  c->prefix_len = P;
+  c->prefix_batch = batch;
+  c->prefix_set = true;
+  return UAD_OK;
+}
+
+static uad_status check_step_args(uad_ctx *c, const void *x, const void *t, const void *dt, const void *mask,
+                                  int B, int H, const char *fn) {
+  if (!x || !t || !dt || !mask) return fail(c, UAD_E_INVALID, std::string(fn) + ": null x/t/dt/mask");
+  if (B < 1 || H < 1) return fail(c, UAD_E_INVALID, std::string(fn) + ": batch and chunk must be >= 1");
+  if (B > c->cfg.max_batch || H > c->cfg.max_chunk)
+    return fail(c, UAD_E_SHAPE, std::string(fn) + ": batch/chunk beyond the context maxima");
+  if (!c->dbg) {
+    if (!c->weights_loaded) return fail(c, UAD_E_STATE, std::string(fn) + ": weights not loaded");
+    if (!c->prefix_set) return fail(c, UAD_E_STATE, std::string(fn) + ": prefix K/V not set");
+    if (B > c->prefix_batch) return fail(c, UAD_E_STATE, std::string(fn) + ": prefix set for fewer environments");
+  }
+  return UAD_OK;
+}
+
+// Enqueue one joint step: F_theta over all B*H tokens, then the masked Euler update.
+static uad_status enqueue_step(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
+                               const uint8_t *next_mask, int is_last, int step, float *v_out, float *released,
+                               int32_t *release_step, int B, int H) {
+  const int M = B * H, d = c->d;
+  hipStream_t s = c->stream;
+  hipError_t e = hipSuccess;
+#define UAD_CHECK_CLS(cls, call)                       \
+  do {                                                 \
+    hipEvent_t ea_ = nullptr, eb_ = nullptr;           \
+    if (c->prof_on) {                                  \
+      ea_ = pool_event(c);                             \
+      eb_ = pool_event(c);                             \
+      (void)hipEventRecord(ea_, s);                    \
+    }                                                  \
+    e = (call);                                        \
+    if (e != hipSuccess) return hip_fail(c, e, #call); \
+    if (c->prof_on) {                                  \
+      (void)hipEventRecord(eb_, s);                    \
+      c->prof_pending.push_back({cls, ea_, eb_});      \
+    }                                                  \
+  } while (0)
+  if (!c->dbg) {
+    const size_t MA = c->m_alloc;
+    UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
+                                      MA * 2 * d, s));
+    GemmArgs g{};
+    g.M = M;
+    g.A = c->a_te; g.lda = 2 * d; g.a_plane = MA * 2 * d; g.W = c->t1_w; g.N = d; g.K = 2 * d;
+    g.out = c->a_z; g.ldo = d; g.out_plane = MA * d; g.bias = c->t1_b;
+    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU_BF16, g, s));
+    g.A = c->a_z; g.lda = d; g.a_plane = MA * d; g.W = c->t2_w; g.N = d; g.K = d;
+    g.out = c->h; g.ldo = d; g.out_plane = 0; g.bias = c->t2_b;
+    UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_F32, g, s));
+
+    AttnArgs at{};
+    at.q = c->q; at.ldq = c->q_dim; at.s_alloc = c->s_alloc; at.n_keys = c->prefix_len + H;
+    at.chunk = H; at.n_heads = c->Hq; at.n_kv_heads = c->Hkv; at.group = c->Hq / c->Hkv;
+    at.rows = at.group * H; at.rows_pad = (at.rows + 63) / 64 * 64;
+    at.splits = attn_splits(c, B, H, c->prefix_len, &at.blocks_per_split);
+    at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
+    at.o = c->a_o; at.ldo = c->q_dim; at.o_plane = MA * c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
+
+    for (int l = 0; l < c->L; ++l) {
+      const uad_layer_ptrs &lp = c->layers[l];
+      __bf16 *kc = c->kcache + l * c->kv_layer_elems;
+      __bf16 *vtc = c->vtcache + l * c->kv_layer_elems;
+      UAD_CHECK_CLS(K_RMSNORM, launch_rmsnorm(c->h, lp.attn_norm, c->cfg.rms_eps, M, d, c->a_n, MA * d, s));
+      GemmArgs q{};
+      q.M = M; q.A = c->a_n; q.lda = d; q.a_plane = MA * d; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
+      q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
+      q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
+      UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, s));
+      at.kc = kc; at.vtc = vtc;
+      UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s));
+      GemmArgs o{};
+      o.M = M; o.A = c->a_o; o.lda = c->q_dim; o.a_plane = MA * c->q_dim; o.W = lp.wo; o.N = d; o.K = c->q_dim; o.out = c->h; o.ldo = d;
+      UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, s));
+      UAD_CHECK_CLS(K_RMSNORM, launch_rmsnorm(c->h, lp.mlp_norm, c->cfg.rms_eps, M, d, c->a_n, MA * d, s));
+      GemmArgs gu{};
+      gu.M = M; gu.A = c->a_n; gu.lda = d; gu.a_plane = MA * d; gu.W = lp.wgu; gu.N = 2 * c->F; gu.K = d;
+      gu.out = c->a_g; gu.ldo = c->F; gu.out_plane = MA * c->F;
+      UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU_BF16, gu, s));
+      GemmArgs dn{};
+      dn.M = M; dn.A = c->a_g; dn.lda = c->F; dn.a_plane = MA * c->F; dn.W = lp.wdown; dn.N = d; dn.K = c->F; dn.out = c->h; dn.ldo = d;
+      UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_RESID_F32, dn, s));
+    }
+  }
+  FinalArgs f{};
+  f.h = c->h; f.gain = c->final_norm; f.w_out = c->action_out_w; f.b_out = c->action_out_b; f.eps = c->cfg.rms_eps;
+  f.M = M; f.d = d; f.Da = c->Da; f.x = x; f.t = t; f.dt = dt; f.mask = mask; f.next_mask = next_mask;
+  f.is_last_step = is_last; f.step = step; f.v_out = v_out; f.released = released; f.release_step = release_step;
+  f.debug_field = c->dbg ? 1 : 0; f.dbg_alpha = c->dbg_alpha; f.dbg_beta = c->dbg_beta;
+  UAD_CHECK_CLS(K_FINAL, launch_final(f, s));
+#undef UAD_CHECK_CLS
+  return UAD_OK;
+}
+
+uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
+                            float *v_out, int32_t batch, int32_t chunk) {
+  if (!c) return UAD_E_INVALID;
+  uad_status st = check_step_args(c, x, t, dt, mask, batch, chunk, "uad_denoise_step");
+  if (st != UAD_OK) return st;
+  (void)hipSetDevice(c->device);
+  return enqueue_step(c, x, t, dt, mask, nullptr, 0, 0, v_out, nullptr, nullptr, batch, chunk);
+}
+
+uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, const float *dt_sched,
+                                const uint8_t *mask_sched, int32_t n_steps, int32_t batch, int32_t chunk,
+                                float *released, int32_t *release_step, uint64_t *step_ticks) {
+  if (!c) return UAD_E_INVALID;
+  uad_status st = check_step_args(c, x, t_sched, dt_sched, mask_sched, batch, chunk, "uad_denoise_schedule");
+  if (st != UAD_OK) return st;
+  if (n_steps < 1) return fail(c, UAD_E_INVALID, "uad_denoise_schedule: n_steps must be >= 1");
+  (void)hipSetDevice(c->device);
+  const size_t M = (size_t)batch * chunk;
+  if (step_ticks) {
+    hipError_t e = launch_stamp(step_ticks, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
+  }
+  for (int k = 0; k < n_steps; ++k) {
+    const bool last = k == n_steps - 1;
+    st = enqueue_step(c, x, t_sched + k * M, dt_sched + k * M, mask_sched + k * M,
+                      last ? nullptr : mask_sched + (k + 1) * M, last ? 1 : 0, k, nullptr, released, release_step,
+                      batch, chunk);
+    if (st != UAD_OK) return st;
+    if (step_ticks) {
+      hipError_t e = launch_stamp(step_ticks + k + 1, c->stream);
+      if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
+    }
+  }
+  return UAD_OK;
+}
+
+uad_status uad_synchronize(uad_ctx *c) {
+  if (!c) return UAD_E_INVALID;
+  (void)hipSetDevice(c->device);
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+  return UAD_OK;
+}
+
+uad_status uad_tick_rate_hz(uad_ctx *c, double *hz) {
+  if (!c || !hz) return UAD_E_INVALID;
+  *hz = c->tick_hz;
+  return UAD_OK;
+}
+
+uad_status uad_debug_velocity_field(uad_ctx *c, int32_t enable, float alpha, float beta) {
+  if (!c) return UAD_E_INVALID;
+  c->dbg = enable != 0;
+  c->dbg_alpha = alpha;
+  c->dbg_beta = beta;
+  return UAD_OK;
+}
+
+uad_status uad_profile_enable(uad_ctx *c, int32_t enable) {
+  if (!c) return UAD_E_INVALID;
+  (void)hipSetDevice(c->device);
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+  for (auto &r : c->prof_pending) {
+    c->ev_pool.push_back(r.a);
+    c->ev_pool.push_back(r.b);
+  }
+  c->prof_pending.clear();
+  c->prof_ms.assign(K_NCLASS, 0.0);
+  c->prof_n.assign(K_NCLASS, 0);
+  c->prof_on = enable != 0;
+  return UAD_OK;
+}
+
+uad_status uad_profile_read(uad_ctx *c, int32_t index, char *name, int32_t name_cap, double *total_ms,
+                            int64_t *launches) {
+  if (!c) return UAD_E_INVALID;
+  if (index < 0 || index >= K_NCLASS) return fail(c, UAD_E_INVALID, "uad_profile_read: index out of range");
+  (void)hipSetDevice(c->device);
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+  if (c->prof_ms.size() != K_NCLASS) {
+    c->prof_ms.assign(K_NCLASS, 0.0);
+    c->prof_n.assign(K_NCLASS, 0);
+  }
+  for (auto &r : c->prof_pending) {
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
+    c->prof_ms[r.cls] += ms;
+    c->prof_n[r.cls] += 1;
+    c->ev_pool.push_back(r.a);
+    c->ev_pool.push_back(r.b);
+  }
+  c->prof_pending.clear();
+  if (name && name_cap > 0) {
+    std::strncpy(name, kClassNames[index], name_cap - 1);
+    name[name_cap - 1] = 0;
+  }
+  if (total_ms) *total_ms = c->prof_ms[index];
+  if (launches) *launches = c->prof_n[index];
+  return UAD_OK;
+}
+
+uad_status uad_build_schedule(const int32_t *budgets, int32_t batch, int32_t chunk, int32_t max_steps,
+                              int32_t *n_steps, float *t, float *dt, uint8_t *mask) {
+  std::string err;
+  return build_schedule_host(budgets, batch, chunk, max_steps, n_steps, t, dt, mask, &err) ? UAD_OK
+                                                                                           : UAD_E_INVALID;
+}
+
+}  // extern "C"

@@ -1,0 +1,182 @@
+// Internal declarations shared by the translation units of libuad.
+// Not part of the public ABI (see include/uad.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/uad.h"
+
+namespace uad {
+
+// ---------------------------------------------------------------------------
+// Vector types for the gfx950 bf16 MFMA builtins
+// ---------------------------------------------------------------------------
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+// Packed weight layout used by every MFMA GEMM ("fragment order"):
+// a row-major W[N][K] (PyTorch [out][in]) is cut into 16x32 blocks; block
+// (nt, kb) holds 64 lanes x 8 consecutive-k bf16 values, lane l carrying
+// W[16*nt + (l & 15)][32*kb + 8*(l >> 4) + e], e = 0..7.  Blocks are stored
+// n-tile major, so one 16-column tile's whole K stream is contiguous and each
+// lane's operand is one aligned 16-byte load.
+constexpr int kTileN = 16;
+constexpr int kTileK = 32;
+constexpr int kBlockElems = kTileN * kTileK;  // 512 bf16 = 1 KiB
+
+// GEMM activation operands are carried as two bf16 planes, hi = bf16(a) and
+// lo = bf16(a - hi), stored `plane` elements apart; the GEMMs multiply both
+// planes by the same bf16 weight fragment.  This keeps ~16 significant bits
+// of every activation while the weights (bf16 by definition) are read once.
+__device__ __forceinline__ void store_split(__bf16 *hi, size_t plane, float v) {
+  const __bf16 h = (__bf16)v;
+  hi[0] = h;
+  hi[plane] = (__bf16)(v - (float)h);
+}
+
+// ---------------------------------------------------------------------------
+// Kernel argument blocks
+// ---------------------------------------------------------------------------
+enum Epilogue : int {
+  EPI_BIAS_SILU_BF16 = 0,  // out bf16 = silu(acc + bias)
+  EPI_BIAS_F32 = 1,        // out fp32 = acc + bias
+  EPI_RESID_F32 = 2,       // out fp32 += acc
+  EPI_GEGLU_BF16 = 3,      // out bf16 = gelu_tanh(acc_gate) * acc_up (tile-interleaved gate/up)
+  EPI_QKV = 4,             // q -> bf16 q buffer; k, v -> per-layer K / V^T store
+};
+
+struct GemmArgs {
+  const __bf16 *A;  // activations, hi plane [>= round_up(M,64)][lda] bf16
+  int lda;
+  size_t a_plane;   // element offset of the lo plane
+  size_t out_plane; // element offset of the lo plane of a split bf16 output
+  const __bf16 *W;  // packed weights, N/16 tiles x K/32 blocks
+  int M, N, K;      // N counts packed output columns (2F for gate/up)
+  void *out;        // epilogue destination
+  int ldo;
+  const float *bias;
+  // EPI_QKV destinations
+  __bf16 *kc;   // layer K store [B][Hkv][S_alloc][hd]
+  __bf16 *vtc;  // layer V^T store [B][Hkv][hd][S_alloc]
+  int chunk, prefix, s_alloc, n_kv_heads, head_dim, q_dim;
+};
+
+struct AttnArgs {
+  const __bf16 *q;  // [M][ldq] bf16, query head j at columns j*hd
+  int ldq;
+  const __bf16 *kc;  // layer K store
+  const __bf16 *vtc; // layer V^T store
+  int s_alloc;
+  int n_keys;        // prefix + chunk
+  int chunk, n_heads, n_kv_heads, group, rows, rows_pad;
+  int splits, blocks_per_split;
+  float scale_log2;  // log2(e) / sqrt(hd)
+  __bf16 *o;         // [M][ldo] bf16, hi plane (lo plane o_plane elements further)
+  int ldo;
+  size_t o_plane;
+  float *opart;      // [splits][B*Hkv][rows_pad][hd] (splits > 1)
+  float *mlpart;     // [splits][B*Hkv][rows_pad][2]
+};
+
+struct FinalArgs {
+  const float *h;       // [M][d]
+  const float *gain;    // final_norm [d]
+  const float *w_out;   // [Da][d] fp32
+  const float *b_out;   // [Da]
+  float eps;
+  int M, d, Da;
+  float *x;             // [M][Da] in/out
+  const float *t, *dt;  // [M]
+  const uint8_t *mask;  // [M]
+  const uint8_t *next_mask;  // [M] or null (schedule: mask of the next step)
+  int is_last_step;
+  int step;
+  float *v_out;         // [M][Da] or null
+  float *released;      // [M][Da] or null
+  int32_t *release_step;// [M] or null
+  int debug_field;
+  float dbg_alpha, dbg_beta;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (defined in the .hip translation units)
+// ---------------------------------------------------------------------------
+hipError_t launch_gemm(int epi, const GemmArgs &g, hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s);
+hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
+                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s);
+hipError_t launch_rmsnorm(const float *h, const float *gain, float eps, int M, int d, __bf16 *out,
+                          size_t plane, hipStream_t s);
+hipError_t launch_final(const FinalArgs &f, hipStream_t s);
+hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
+
+// Host-side helpers (schedule.cpp)
+bool build_schedule_host(const int32_t *budgets, int batch, int chunk, int max_steps, int32_t *n_steps,
+                         float *t, float *dt, uint8_t *mask, std::string *err);
+
+}  // namespace uad
+
+// ---------------------------------------------------------------------------
+// Context
+// ---------------------------------------------------------------------------
+struct uad_layer_ptrs {
+  const __bf16 *wqkv, *wo, *wgu, *wdown;
+  const float *attn_norm, *mlp_norm;
+};
+
+struct uad_ctx {
+  uad_model_config cfg{};
+  int device = 0;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  std::string err;
+
+  int d = 0, L = 0, Hq = 0, Hkv = 0, hd = 0, F = 0, Da = 0;
+  int q_dim = 0, kv_dim = 0, n_qkv = 0;
+  int m_alloc = 0;   // activation rows, multiple of 64 (split buffers: 2 planes of m_alloc rows)
+  int s_alloc = 0;   // key slots per (layer, env, kv head), multiple of 32
+
+  // weights
+  void *wbuf = nullptr;
+  size_t wbytes = 0;
+  float *action_in_w = nullptr, *action_in_b = nullptr, *t1_b = nullptr, *t2_b = nullptr;
+  float *final_norm = nullptr, *action_out_w = nullptr, *action_out_b = nullptr, *freqs = nullptr;
+  __bf16 *t1_w = nullptr, *t2_w = nullptr;
+  std::vector<uad_layer_ptrs> layers;
+  bool weights_loaded = false;
+
+  // prefix / chunk K,V store
+  __bf16 *kcache = nullptr, *vtcache = nullptr;
+  size_t kv_layer_elems = 0;  // elements per layer in each store
+  int prefix_len = 0, prefix_batch = 0;
+  bool prefix_set = false;
+
+  // activation workspace
+  float *h = nullptr;
+  __bf16 *a_te = nullptr, *a_z = nullptr, *a_n = nullptr, *a_o = nullptr, *a_g = nullptr, *q = nullptr;
+  float *attn_opart = nullptr, *attn_ml = nullptr;
+  size_t attn_part_elems = 0;
+  void *abuf = nullptr;
+
+  // measurement hook: events around every launch, grouped by kernel class
+  struct ProfRec {
+    int cls;
+    hipEvent_t a, b;
+  };
+  bool prof_on = false;
+  std::vector<ProfRec> prof_pending;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<double> prof_ms;
+  std::vector<int64_t> prof_n;
+
+  // test hook
+  bool dbg = false;
+  float dbg_alpha = 0.f, dbg_beta = 0.f;
+  double tick_hz = 0.0;
+};

@@ -1,0 +1,228 @@
+"""GPU parity of the libuad hot path against the CPU oracle, through the C ABI.
+
+Bars: per-step velocities within a normwise max relative error of 2e-2
+(teacher-forced: the GPU step gets the oracle's state, times and mask), final
+and released actions within 1e-2 absolute (free-running schedule), schedule
+tables, masks and release steps bit-exact, frozen tokens bit-identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import uad_workloads as W
+from tests.harness import log, make_case, rel_err
+
+pytestmark = pytest.mark.gpu
+
+VEL_RTOL = 2e-2
+ACT_ATOL = 1e-2
+
+_cases = {}
+
+
+def case(name, **kw):
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cases:
+        _cases[key] = make_case(name, **kw)
+    return _cases[key]
+
+
+def dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t if dtype is None else t.to(dtype)
+
+
+def gpu_velocity(c, x, t, dt, mask):
+    """One GPU step on given inputs; returns (x_after, v)."""
+    xg = dev(x.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t.astype(np.float32)), dev(dt.astype(np.float32)), dev(mask.astype(np.uint8)), vg)
+    torch.cuda.synchronize()
+    return xg.cpu().numpy(), vg.cpu().numpy()
+
+
+def run_schedule_gpu(c, x0, budgets):
+    n, tg, dtg, mg = c.expert.schedule_tables(budgets)
+    xg = dev(x0.astype(np.float32))
+    rel = torch.zeros_like(xg)
+    rst = torch.full(budgets.shape, -1, dtype=torch.int32, device="cuda")
+    c.expert.schedule(xg, tg, dtg, mg, rel, rst)
+    torch.cuda.synchronize()
+    return xg.cpu().numpy(), rel.cpu().numpy(), rst.cpu().numpy()
+
+
+# ----------------------------------------------------------------------------
+# Teacher-forced velocities + free-running schedules, per workload
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("name,steps", [("tiny", None), ("pi0_b1", [0, 5, 9]), ("pi0_b1_uad", [0, 4, 8])])
+def test_teacher_forced_velocity(gpu, name, steps):
+    c = case(name)
+    m = c.oracle_model()
+    r = O.denoise_schedule(m, c.noise, c.budgets, keep_history=True)
+    ks = range(r["n_steps"]) if steps is None else steps
+    for k in ks:
+        x_in, v_ref = r["history"][k]
+        _, v = gpu_velocity(c, x_in, r["t"][k], r["dt"][k], r["mask"][k])
+        for b in range(c.wl.batch):
+            e = rel_err(v[b], v_ref[b])
+            log(f"[{name}] step {k} env {b}: velocity rel err {e:.2e}")
+            assert e <= VEL_RTOL
+
+
+@pytest.mark.parametrize("name", ["tiny", "pi0_b1", "pi0_b1_uad"])
+def test_free_running_schedule(gpu, name):
+    c = case(name)
+    r = O.denoise_schedule(c.oracle_model(), c.noise, c.budgets)
+    x, rel, rst = run_schedule_gpu(c, c.noise, c.budgets)
+    err_x = float(np.max(np.abs(x - r["x"])))
+    err_rel = float(np.max(np.abs(rel - r["released"])))
+    log(f"[{name}] final max abs err {err_x:.2e}, released {err_rel:.2e}")
+    assert err_x <= ACT_ATOL and err_rel <= ACT_ATOL
+    np.testing.assert_array_equal(rst, r["release_step"])
+    # released actions of a token equal its final state (frozen afterwards)
+    assert rel.tobytes() == x.tobytes()
+
+
+def test_fleet_sampled_envs(gpu):
+    """64 environments, per-env random budgets: sampled envs against the oracle run alone."""
+    c = case("pi0_fleet_b64")
+    B = c.wl.batch
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    # one teacher-forced joint step at k=0 for every env, sampled comparison
+    _, v = gpu_velocity(c, c.noise, t[0], dt[0], mask[0])
+    x, rel, rst = run_schedule_gpu(c, c.noise, c.budgets)
+    for b in (0, 17, 40, B - 1):
+        mb = c.oracle_model([b])
+        v_ref = O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0]
+        e = rel_err(v[b], v_ref)
+        r = O.denoise_schedule(mb, c.noise[b:b + 1], c.budgets[b:b + 1])
+        ea = float(np.max(np.abs(rel[b] - r["released"][0])))
+        log(f"[fleet] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
+        assert e <= VEL_RTOL and ea <= ACT_ATOL
+        np.testing.assert_array_equal(rst[b], r["release_step"][0])
+    np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
+
+
+def test_large_sampled_envs(gpu):
+    """24 layers, width 1536, GQA 12/2, H=128, B=16: sampled envs at two schedule steps."""
+    c = case("large_b16")
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    r_env = {}
+    for b in (0, 15):
+        r_env[b] = O.denoise_schedule(c.oracle_model([b]), c.noise[b:b + 1], c.budgets[b:b + 1], keep_history=True)
+    for k in (0, 7):
+        x_in = c.noise.copy()
+        for b in r_env:
+            x_in[b] = r_env[b]["history"][k][0][0]
+        _, v = gpu_velocity(c, x_in, t[k], dt[k], mask[k])
+        for b in r_env:
+            e = rel_err(v[b], r_env[b]["history"][k][1][0])
+            log(f"[large] step {k} env {b}: velocity rel err {e:.2e}")
+            assert e <= VEL_RTOL
+    x, rel, rst = run_schedule_gpu(c, c.noise, c.budgets)
+    for b in r_env:
+        ea = float(np.max(np.abs(rel[b] - r_env[b]["released"][0])))
+        log(f"[large] env {b}: released abs err {ea:.2e}")
+        assert ea <= ACT_ATOL
+
+
+# ----------------------------------------------------------------------------
+# Invariants of the method on the GPU path
+# ----------------------------------------------------------------------------
+def test_uniform_schedule_equals_repeated_vanilla_steps_bit_exact(gpu):
+    c = case("tiny")
+    N = 10
+    x, _, _ = run_schedule_gpu(c, c.noise, np.full_like(c.budgets, N))
+    xg = dev(c.noise.astype(np.float32))
+    B, H = c.budgets.shape
+    for k in range(N):
+        tk = np.full((B, H), np.float32(N - k) / np.float32(N), np.float32)
+        dtk = np.full((B, H), -(np.float32(1) / np.float32(N)), np.float32)
+        c.expert.step(xg, dev(tk), dev(dtk), dev(np.zeros((B, H), np.uint8)))
+    torch.cuda.synchronize()
+    assert xg.cpu().numpy().tobytes() == x.tobytes()
+
+
+def test_frozen_tokens_bit_identical_on_gpu(gpu):
+    c = case("pi0_b1_uad")
+    n, tg, dtg, mg = c.expert.schedule_tables(c.budgets)
+    x0 = c.noise.astype(np.float32).copy()
+    x0[0, 0, 0] = -0.0
+    xg = dev(x0)
+    snaps = []
+    for k in range(n):
+        c.expert.step(xg, tg[k], dtg[k], mg[k])
+        torch.cuda.synchronize()
+        snaps.append(xg.cpu().numpy().copy())
+    for i, N in enumerate(c.budgets[0]):
+        for k in range(N, n):
+            assert snaps[k][0, i].tobytes() == snaps[N - 1][0, i].tobytes()
+
+
+def test_nan_velocity_never_reaches_frozen_tokens(gpu):
+    c = case("tiny")
+    B, H, Da = c.noise.shape
+    x0 = c.noise.astype(np.float32).copy()
+    x0[0, 1, :] = -0.0
+    mask = np.zeros((B, H), np.uint8)
+    mask[0, :4] = 1
+    dt = np.full((B, H), -0.1, np.float32)
+    dt[0, 4:6] = 0.0
+    c.expert.debug_velocity_field(True, 0.0, float("nan"))
+    try:
+        x1, v = gpu_velocity(c, x0, np.ones((B, H), np.float32), dt, mask)
+    finally:
+        c.expert.debug_velocity_field(False)
+    assert x1[0, :6].tobytes() == x0[0, :6].tobytes()
+    assert np.all(np.isnan(x1[0, 6:])) and np.all(np.isnan(v))
+
+
+@pytest.mark.parametrize("alpha,beta", [(0.0, 0.7), (0.35, -0.2), (-1.3, 0.5)])
+def test_linear_field_closed_form_on_gpu(gpu, alpha, beta):
+    c = case("pi0_b1_uad")
+    c.expert.debug_velocity_field(True, alpha, beta)
+    try:
+        x, rel, rst = run_schedule_gpu(c, c.noise, c.budgets)
+    finally:
+        c.expert.debug_velocity_field(False)
+    N = c.budgets.astype(np.float64)[..., None]
+    dtv = -1.0 / N
+    g = (1.0 + alpha * dtv) ** N
+    ref = g * c.noise + (beta * (g - 1.0) / alpha if alpha != 0 else beta * N * dtv)
+    np.testing.assert_allclose(rel, ref, rtol=2e-6, atol=2e-6)
+    np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
+
+
+def test_run_to_run_determinism(gpu):
+    c = case("pi0_b1_uad")
+    a = run_schedule_gpu(c, c.noise, c.budgets)
+    b = run_schedule_gpu(c, c.noise, c.budgets)
+    for u, w in zip(a, b):
+        assert u.tobytes() == w.tobytes()
+
+
+# ----------------------------------------------------------------------------
+# Edge cases: ragged chunks, no prefix, single token, batch subsets
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("H,P", [(1, 64), (37, 0), (16, 1), (45, 97)])
+def test_ragged_chunk_and_prefix(gpu, H, P):
+    c = case("tiny", chunk=H, prefix=P, batch=2)
+    m = c.oracle_model()
+    n, t, dt, mask = O.build_schedule(np.array([[3] * H, [1 + (i % 4) for i in range(H)]]))
+    x_in = c.noise
+    v_ref = O.velocity(m, x_in, t[1])
+    _, v = gpu_velocity(c, x_in, t[1], dt[1], mask[1])
+    for b in range(2):
+        e = rel_err(v[b], v_ref[b])
+        log(f"[ragged H={H} P={P}] env {b}: velocity rel err {e:.2e}")
+        assert e <= VEL_RTOL
+
+
+def test_batch_subset_matches_full_batch(gpu):
+    """A call with fewer environments than the prefix holds uses the first ones."""
+    c = case("tiny", batch=3)
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    _, v3 = gpu_velocity(c, c.noise, t[2], dt[2], mask[2])
+    _, v1 = gpu_velocity(c, c.noise[:1], t[2][:1], dt[2][:1], mask[2][:1])
+    assert rel_err(v1[0], v3[0]) <= 1e-3
