@@ -176,8 +176,9 @@ def main():
     ms_step = 1e3 * el / steps
     log(f"[bench] timed {steps} steps: {ms_step:.4f} ms/step, {sps:.1f} steps/s")
 
-    # Per-kernel durations: the same schedules again with HIP events around every launch
-    # (recorded by the library on the stream its kernels run on).
+    # Per-kernel durations: the same schedules again, launched directly with a
+    # start/stop HIP event pair taken from each kernel's dispatch packet, on the
+    # stream the kernels run on (the library's measurement hook).
     U.uad_profile_enable(ex.ctx, True)
     run(n_timed)
     prof = U.uad_profile_read(ex.ctx)
@@ -237,7 +238,7 @@ def main():
 
 
 def availability(ex, wl, noise, U, np, torch, reps=20):
-    """Release times of the S executed actions and AAL (App. B / App. D.3) for the
+    """Release times of the S executed actions and AAL (App. B / App. C.3) for the
     vanilla uniform schedule and the UAD 4/7/10 schedule on this model."""
     import uad_workloads as W
     hz = ex.tick_rate_hz()

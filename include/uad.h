@@ -172,7 +172,7 @@ uad_status uad_build_schedule(const int32_t *budgets, int32_t batch, int32_t chu
 
 /* Average action-availability latency of a controller that executes actions in
  * order, each for t_act, starting each action as soon as it is released and
- * the previous one finished (App. B timing model, App. D.3 measurement):
+ * the previous one finished (App. B timing model, App. C.3 measurement):
  * AAL = (sum of waits) / n.  release[j] is the release time of executed
  * action j measured from the request.  Pure host code. */
 uad_status uad_aal(const double *release, int32_t n, double t_act, double *aal_out);

@@ -20,7 +20,7 @@ What it computes, in the paper's order and notation:
   Ghost Action Correction on additive dimensions (Sec. 4.4, Eqs. 8-9).
 * The latency model of App. B (Eqs. latency_vanilla / latency_uaer) and an
   availability-latency controller that replays release times against the
-  per-action execution budget T_act (App. D.3).
+  per-action execution budget T_act (App. C.3).
 
 Readings where the paper is silent (each is also listed in the design notes):
 
@@ -347,7 +347,7 @@ def gac_correct(released: np.ndarray, ghosts: np.ndarray, tail: np.ndarray,
 
 
 # ----------------------------------------------------------------------------
-# Availability latency (App. B; App. D.3)
+# Availability latency (App. B; App. C.3)
 # ----------------------------------------------------------------------------
 def latency_vanilla(T_vlm: float, T_D: float, Nstar: int, S: int) -> float:
     """Average action-availability latency of vanilla inference (Eq. latency_vanilla)."""
@@ -365,7 +365,7 @@ def aal_controller(release_times: Sequence[float], T_act: float) -> float:
     Action j can start once it is released (release_times[j], measured from the
     request) and the previous action finished; the wait before each start is
     the exposed latency.  Returns the total wait divided by the number of
-    executed actions (AAL, App. D.3).
+    executed actions (AAL, App. C.3).
     """
     clock = 0.0
     wait = 0.0

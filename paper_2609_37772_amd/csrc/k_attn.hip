@@ -7,7 +7,8 @@
 //
 // Per workgroup: one (environment, KV head), 64 packed query rows (4 waves x
 // 16), and a contiguous range of 32-key blocks (split-KV when the batch is
-// small).  K and V^T blocks are staged in LDS and shared by the 4 waves.
+// small).  K and V^T blocks are staged in LDS and shared by the 4 waves; the
+// next block's global loads are issued before the current block is used.
 // Each wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 so that a
 // lane ends up holding 8 scores of ONE query, which are exactly the 8 k-values
 // of its operand for the P V product: no transpose through LDS.  Softmax
@@ -71,22 +72,47 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   int blk1 = blk0 + a.blocks_per_split;
   if (blk1 > n_blocks) blk1 = n_blocks;
 
+  // K/V blocks are prefetched into registers one block ahead, so the global
+  // loads of block b+1 are in flight while block b is multiplied from LDS.
+  constexpr int KCH = 32 * HD / 8 / 256;  // 16-byte K chunks per thread
+  constexpr int VCH = HD * 4 / 256;       // 16-byte V^T chunks per thread
+  bf16x8 kreg[KCH], vreg[VCH];
+  auto fetch = [&](int blk) {
+    const int k0 = blk * 32;
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int row = c / (HD / 8), col = (c - row * (HD / 8)) * 8;
+      kreg[i] = *(const bf16x8 *)(kbase + (size_t)(k0 + row) * HD + col);
+    }
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int row = c >> 2, col = (c & 3) * 8;
+      vreg[i] = *(const bf16x8 *)(vbase + (size_t)row * a.s_alloc + k0 + col);
+    }
+  };
+  if (blk0 < blk1) fetch(blk0);
+
   for (int blk = blk0; blk < blk1; ++blk) {
     const int k0 = blk * 32;
-    __syncthreads();  // previous tile fully consumed
-    // stage K[k0..k0+31][0..HD) : 32*HD/8 chunks of 16 B
-    for (int c = threadIdx.x; c < 32 * HD / 8; c += 256) {
+    __syncthreads();  // previous block fully consumed
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = threadIdx.x + 256 * i;
       const int row = c / (HD / 8), col = (c - row * (HD / 8)) * 8;
-      *(bf16x8 *)&sm.k[row][col] = *(const bf16x8 *)(kbase + (size_t)(k0 + row) * HD + col);
+      *(bf16x8 *)&sm.k[row][col] = kreg[i];
     }
-    // stage V^T[0..HD)[k0..k0+31] : HD*4 chunks of 16 B, written as 2 x 8 B
-    for (int c = threadIdx.x; c < HD * 4; c += 256) {
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = threadIdx.x + 256 * i;
       const int row = c >> 2, col = (c & 3) * 8;
-      const bf16x8 v = *(const bf16x8 *)(vbase + (size_t)row * a.s_alloc + k0 + col);
+      const bf16x8 v = vreg[i];
       *(bf16x4 *)&sm.vt[row][col] = bf16x4{v[0], v[1], v[2], v[3]};
       *(bf16x4 *)&sm.vt[row][col + 4] = bf16x4{v[4], v[5], v[6], v[7]};
     }
     __syncthreads();
+    if (blk + 1 < blk1) fetch(blk + 1);
 
     // S^T for two 16-key halves: s[h][r] = score(query lane&15, key k0+16h+4(lane>>4)+r)
     f32x4 s[2];
@@ -163,10 +189,12 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       if (row >= a.rows) continue;
       const int hg = row / a.chunk, tok = row - hg * a.chunk;
       const int head = g * a.group + hg;
-      __bf16 *op = a.o + (size_t)(b * a.chunk + tok) * a.ldo + head * HD + (lane & 15);
+      const int orow = b * a.chunk + tok;
       const float inv = 1.0f / lr[r];
 #pragma unroll
-      for (int nt = 0; nt < NTO; ++nt) store_split(op + nt * 16, a.o_plane, o[nt][r] * inv);
+      for (int nt = 0; nt < NTO; ++nt)
+        store_split(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), a.o_plane,
+                    o[nt][r] * inv);
     }
   } else {
     const size_t pbase = ((size_t)split * gridDim.z + eh) * a.rows_pad;
@@ -185,43 +213,63 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
-// Merge split-KV partials: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+// Merge split-KV partials: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
+// splits in fixed order.  The (m_s, l_s) pairs of the row are staged in LDS
+// by one vector load per thread; every partial load is issued up front.
+constexpr int kMaxKvSplits = 32;
 template <int HD>
 __global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a) {
+  __shared__ float2 mls[kMaxKvSplits];
   const int row = blockIdx.x;
   const int eh = blockIdx.y;
   const int b = eh / a.n_kv_heads, g = eh - b * a.n_kv_heads;
   const int c = threadIdx.x;
   const int n_eh = gridDim.y;
+  const int splits = a.splits;
+  const float *__restrict__ opart = a.opart;
+  if (c < kMaxKvSplits)
+    mls[c] = c < splits ? *(const float2 *)(a.mlpart + (((size_t)c * n_eh + eh) * a.rows_pad + row) * 2)
+                        : float2{-INFINITY, 0.f};
+  float os[kMaxKvSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxKvSplits; ++s)
+    os[s] = s < splits ? opart[(((size_t)s * n_eh + eh) * a.rows_pad + row) * HD + c] : 0.f;
+  __syncthreads();
   float M = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) M = fmaxf(M, a.mlpart[(((size_t)s * n_eh + eh) * a.rows_pad + row) * 2]);
+#pragma unroll
+  for (int s = 0; s < kMaxKvSplits; ++s) M = fmaxf(M, mls[s].x);
   float num = 0.f, den = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    const size_t base = ((size_t)s * n_eh + eh) * a.rows_pad + row;
-    const float w = exp2f(a.mlpart[base * 2] - M);
-    num += w * a.opart[base * HD + c];
-    den += w * a.mlpart[base * 2 + 1];
+#pragma unroll
+  for (int s = 0; s < kMaxKvSplits; ++s) {
+    if (s < splits) {
+      const float w = exp2f(mls[s].x - M);
+      num += w * os[s];
+      den += w * mls[s].y;
+    }
   }
   const int hg = row / a.chunk, tok = row - hg * a.chunk;
   const int head = g * a.group + hg;
-  store_split(a.o + (size_t)(b * a.chunk + tok) * a.ldo + head * HD + c, a.o_plane, num / den);
+  store_split(a.o + afrag_index(b * a.chunk + tok, head * HD + c, a.ldo / kTileK), a.o_plane, num / den);
 }
 
 template <int HD>
-static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s) {
+static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   dim3 grid((a.rows + 63) / 64, a.splits, batch * a.n_kv_heads);
-  hipLaunchKernelGGL((attn_kernel<HD>), grid, dim3(256), 0, s, a);
+  hipEvent_t end_attn = a.splits == 1 ? ev1 : nullptr;
+  UAD_LAUNCH((attn_kernel<HD>), grid, dim3(256), 0, s, ev0, end_attn, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  hipLaunchKernelGGL((attn_combine_kernel<HD>), dim3(a.rows, batch * a.n_kv_heads), dim3(HD), 0, s, a);
+  hipEvent_t none = nullptr;
+  UAD_LAUNCH((attn_combine_kernel<HD>), dim3(a.rows, batch * a.n_kv_heads), dim3(HD), 0, s, none, ev1, a);
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s) {
+hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0,
+                            hipEvent_t ev1) {
   switch (head_dim) {
-    case 64: return launch_hd<64>(a, batch, s);
-    case 128: return launch_hd<128>(a, batch, s);
-    case 256: return launch_hd<256>(a, batch, s);
+    case 64: return launch_hd<64>(a, batch, s, ev0, ev1);
+    case 128: return launch_hd<128>(a, batch, s, ev0, ev1);
+    case 256: return launch_hd<256>(a, batch, s, ev0, ev1);
   }
   return hipErrorInvalidValue;
 }

@@ -1,9 +1,11 @@
-// Small per-token kernels of the step: the per-token time embedding and
-// action input projection, RMSNorm to bf16 GEMM operands, and the final
-// norm + action projection fused with the masked per-token Euler update.
+// Per-token kernels of the step: the per-token time embedding and action
+// input projection, the K-split reduction fused with the residual add and the
+// next RMSNorm, and the final norm + action projection fused with the masked
+// per-token Euler update.
 #include "uad_internal.h"
 
 namespace uad {
+
 
 // Sum over a 256-thread block in a fixed order (wave shuffles, then 4 partials).
 __device__ __forceinline__ float block_sum_256(float v, float *scratch) {
@@ -16,8 +18,9 @@ __device__ __forceinline__ float block_sum_256(float v, float *scratch) {
   return (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
 }
 
-// te[m] = [ x_m W_in^T + b_in ; sin(w t_m) ; cos(w t_m) ] as split bf16 planes
-// (per-token flow-time conditioning before the action MLP)
+// te[m] = [ x_m W_in^T + b_in ; sin(w t_m) ; cos(w t_m) ] as split bf16 planes in
+// fragment order (K = 2d): the per-token flow-time conditioning placed before
+// the action MLP.
 __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, const float *__restrict__ t,
                                                     int Da, int d, const float *__restrict__ w_in,
                                                     const float *__restrict__ b_in,
@@ -25,68 +28,131 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
                                                     size_t plane) {
   __shared__ float xs[64];
   const int m = blockIdx.x;
+  const int KB = 2 * d / kTileK;
   if (threadIdx.x < Da) xs[threadIdx.x] = x[(size_t)m * Da + threadIdx.x];
   __syncthreads();
-  __bf16 *row = te + (size_t)m * 2 * d;
   for (int n = threadIdx.x; n < d; n += blockDim.x) {
     float acc = b_in[n];
     const float *w = w_in + (size_t)n * Da;
     for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
-    store_split(row + n, plane, acc);
+    store_split(te + afrag_index(m, n, KB), plane, acc);
   }
   const float tm = t[m];
   const int half = d >> 1;
   for (int j = threadIdx.x; j < half; j += blockDim.x) {
     const float arg = freqs[j] * tm;
-    store_split(row + d + j, plane, sinf(arg));
-    store_split(row + d + half + j, plane, cosf(arg));
+    store_split(te + afrag_index(m, d + j, KB), plane, sinf(arg));
+    store_split(te + afrag_index(m, d + half + j, KB), plane, cosf(arg));
   }
 }
 
-// out[m] = h[m] / sqrt(mean(h[m]^2) + eps) * gain, as split bf16 planes
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float *__restrict__ h, const float *__restrict__ gain,
-                                                       float eps, int d, __bf16 *__restrict__ out,
-                                                       size_t plane) {
+// Row m: h = (bias | h) + (p_0 + p_1 + ... ) over the S K-split partials of
+// the projection, then (if gain) the next GEMM operand n = RMSNorm(h) * gain.
+// NC = columns per thread (d <= 256*NC).  Every load is unconditional (index
+// clamped into the row, masked afterwards) so all of them issue back to back.
+template <int NC, int S>
+__global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs r) {
   __shared__ float scratch[4];
   const int m = blockIdx.x;
-  const float *hr = h + (size_t)m * d;
+  const int d = r.d;
+  float *__restrict__ hr = r.h + (size_t)m * d;
+  const float *__restrict__ basep = r.bias ? r.bias : hr;  // one pointer: no branch between two loads
+  const float *__restrict__ part = r.part + (size_t)m * d;
+  const size_t pstride = (size_t)r.part_rows * d;
+  float base[NC], pv[S][NC];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = min(threadIdx.x + 256 * i, d - 1);
+    base[i] = basep[c];
+#pragma unroll
+    for (int s2 = 0; s2 < S; ++s2) pv[s2][i] = part[s2 * pstride + c];
+  }
+  float hv[NC];
   float ss = 0.f;
-  for (int k = threadIdx.x; k < d; k += blockDim.x) ss += hr[k] * hr[k];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    float acc = 0.f;
+#pragma unroll
+    for (int s2 = 0; s2 < S; ++s2) acc += pv[s2][i];
+    const bool ok = threadIdx.x + 256 * i < d;
+    hv[i] = ok ? base[i] + acc : 0.f;
+    ss += hv[i] * hv[i];
+  }
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c < d) hr[c] = hv[i];
+  }
+  if (!r.gain) return;
   ss = block_sum_256(ss, scratch);
-  const float rstd = 1.0f / sqrtf(ss / (float)d + eps);
-  __bf16 *orow = out + (size_t)m * d;
-  for (int k = threadIdx.x; k < d; k += blockDim.x) store_split(orow + k, plane, hr[k] * rstd * gain[k]);
+  const float rstd = 1.0f / sqrtf(ss / (float)d + r.eps);
+  const int KB = d / kTileK;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c < d) store_split(r.n + afrag_index(m, c, KB), r.n_plane, hv[i] * rstd * r.gain[c]);
+  }
 }
 
 // v = RMSNorm(h) W_out^T + b_out, then x <- x + dt v unless frozen (mask or
 // dt == 0: copy, so frozen tokens are bit-identical whatever v holds).
+// Workgroup = (token m, group of up to 8 action dims); thread t owns columns
+// t + 256 i of the row for all 8 dims, loads unconditional as above.
+constexpr int kFinalOuts = 8;
+template <int NC>
 __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
   __shared__ float scratch[4];
-  __shared__ float vs[64];
+  __shared__ float wsum[4][kFinalOuts];
+  __shared__ float vs[kFinalOuts];
   const int m = blockIdx.x;
+  const int a0 = blockIdx.y * kFinalOuts;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int d = f.d;
   if (f.debug_field) {
-    if (threadIdx.x < f.Da) vs[threadIdx.x] = f.dbg_alpha * f.x[(size_t)m * f.Da + threadIdx.x] + f.dbg_beta;
+    if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da)
+      vs[threadIdx.x] = f.dbg_alpha * f.x[(size_t)m * f.Da + a0 + threadIdx.x] + f.dbg_beta;
   } else {
-    const float *hr = f.h + (size_t)m * f.d;
-    float ss = 0.f;
-    for (int k = threadIdx.x; k < f.d; k += blockDim.x) ss += hr[k] * hr[k];
-    ss = block_sum_256(ss, scratch);
-    const float rstd = 1.0f / sqrtf(ss / (float)f.d + f.eps);
-    for (int a = wave; a < f.Da; a += 4) {
-      const float *w = f.w_out + (size_t)a * f.d;
-      float acc = 0.f;
-      for (int k = lane; k < f.d; k += 64) acc += (hr[k] * rstd * f.gain[k]) * w[k];
+    const float *__restrict__ hr = f.h + (size_t)m * d;
+    float hv[NC], gv[NC], wv[kFinalOuts][NC];
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-      if (lane == 0) vs[a] = acc + f.b_out[a];
+    for (int i = 0; i < NC; ++i) {
+      const int c = min(threadIdx.x + 256 * i, d - 1);
+      hv[i] = hr[c];
+      gv[i] = f.gain[c];
+#pragma unroll
+      for (int o = 0; o < kFinalOuts; ++o) wv[o][i] = f.w_out[(size_t)min(a0 + o, f.Da - 1) * d + c];
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      if (threadIdx.x + 256 * i >= d) hv[i] = 0.f;
+      ss += hv[i] * hv[i];
+    }
+    ss = block_sum_256(ss, scratch);
+    const float rstd = 1.0f / sqrtf(ss / (float)d + f.eps);
+    float acc[kFinalOuts];
+#pragma unroll
+    for (int o = 0; o < kFinalOuts; ++o) {
+      acc[o] = 0.f;
+#pragma unroll
+      for (int i = 0; i < NC; ++i) acc[o] += (hv[i] * rstd * gv[i]) * wv[o][i];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) acc[o] += __shfl_xor(acc[o], off);
+    }
+    if (lane == 0)
+#pragma unroll
+      for (int o = 0; o < kFinalOuts; ++o) wsum[wave][o] = acc[o];
+    __syncthreads();
+    if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da) {
+      const int o = threadIdx.x;
+      vs[o] = ((wsum[0][o] + wsum[1][o]) + (wsum[2][o] + wsum[3][o])) + f.b_out[a0 + o];
     }
   }
   __syncthreads();
-  if (threadIdx.x < f.Da) {
-    const int a = threadIdx.x;
+  if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da) {
+    const int a = a0 + threadIdx.x;
     const size_t idx = (size_t)m * f.Da + a;
-    const float v = vs[a];
+    const float v = vs[threadIdx.x];
     const float dtm = f.dt[m];
     const bool frozen = (f.mask[m] != 0) || (dtm == 0.0f);
     const float xo = f.x[idx];
@@ -109,19 +175,51 @@ __global__ void stamp_kernel(uint64_t *dst) {
 }
 
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
-                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s) {
-  hipLaunchKernelGGL(temb_kernel, dim3(M), dim3(256), 0, s, x, t, Da, d, w_in, b_in, freqs, te, plane);
+                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s,
+                       hipEvent_t ev0, hipEvent_t ev1) {
+  UAD_LAUNCH(temb_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, plane);
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(const float *h, const float *gain, float eps, int M, int d, __bf16 *out,
-                          size_t plane, hipStream_t s) {
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, s, h, gain, eps, d, out, plane);
+template <int NC>
+static hipError_t launch_reduce_nc(const ReduceArgs &r, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  switch (r.splits) {
+    case 1: UAD_LAUNCH((reduce_kernel<NC, 1>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
+    case 2: UAD_LAUNCH((reduce_kernel<NC, 2>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
+    case 4: UAD_LAUNCH((reduce_kernel<NC, 4>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
+    case 8: UAD_LAUNCH((reduce_kernel<NC, 8>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_final(const FinalArgs &f, hipStream_t s) {
-  hipLaunchKernelGGL(final_kernel, dim3(f.M), dim3(256), 0, s, f);
+hipError_t launch_reduce(const ReduceArgs &r, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  switch ((r.d + 255) / 256) {
+    case 1: return launch_reduce_nc<1>(r, s, ev0, ev1);
+    case 2: return launch_reduce_nc<2>(r, s, ev0, ev1);
+    case 3: return launch_reduce_nc<3>(r, s, ev0, ev1);
+    case 4: return launch_reduce_nc<4>(r, s, ev0, ev1);
+    case 5: return launch_reduce_nc<5>(r, s, ev0, ev1);
+    case 6: return launch_reduce_nc<6>(r, s, ev0, ev1);
+    case 7: return launch_reduce_nc<7>(r, s, ev0, ev1);
+    case 8: return launch_reduce_nc<8>(r, s, ev0, ev1);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const dim3 grid(f.M, (f.Da + kFinalOuts - 1) / kFinalOuts);
+  switch ((f.d + 255) / 256) {
+    case 1: UAD_LAUNCH(final_kernel<1>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 2: UAD_LAUNCH(final_kernel<2>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 3: UAD_LAUNCH(final_kernel<3>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 4: UAD_LAUNCH(final_kernel<4>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 5: UAD_LAUNCH(final_kernel<5>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 6: UAD_LAUNCH(final_kernel<6>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 7: UAD_LAUNCH(final_kernel<7>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    case 8: UAD_LAUNCH(final_kernel<8>, grid, dim3(256), 0, s, ev0, ev1, f); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -1,6 +1,6 @@
 // Host-only helpers of the C ABI: the per-token step tables built from integer
 // budgets (Sec. 4.2, Eqs. 4-5) and the availability-latency controller
-// (App. B timing model, App. D.3 measurement).
+// (App. B timing model, App. C.3 measurement).
 #include <cstdint>
 #include <string>
 

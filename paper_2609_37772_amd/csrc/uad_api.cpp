@@ -94,10 +94,11 @@ struct Carve {
 };
 
 // Kernel classes reported by the measurement hook.
-enum KClass { K_TEMB, K_GEMM_TIME_IN, K_GEMM_TIME_OUT, K_RMSNORM, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP,
+enum KClass { K_TEMB, K_GEMM_TIME_IN, K_GEMM_TIME_OUT, K_REDUCE, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP,
               K_GEMM_DOWN, K_FINAL, K_NCLASS };
-const char *kClassNames[K_NCLASS] = {"temb", "gemm_time_in", "gemm_time_out", "rmsnorm", "gemm_qkv", "attention",
+const char *kClassNames[K_NCLASS] = {"temb", "gemm_time_in", "gemm_time_out", "reduce_norm", "gemm_qkv", "attention",
                                      "gemm_o", "gemm_gateup", "gemm_down", "final_euler"};
+constexpr int kMaxSplits = 8;
 
 hipEvent_t pool_event(uad_ctx *c) {
   if (!c->ev_pool.empty()) {
@@ -114,13 +115,13 @@ int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) {
   const int rows = (c->Hq / c->Hkv) * H;
   const int qblocks = (rows + 63) / 64;
   const int n_blocks = (P + H + 31) / 32;
+  // split the keys until the grid covers the chip, at >= 2 key blocks per split
   const int wgs = qblocks * B * c->Hkv;
-  int want = (256 + wgs - 1) / wgs;
-  int maxs = n_blocks / 4;
-  if (maxs < 1) maxs = 1;
-  if (want > maxs) want = maxs;
-  if (want < 1) want = 1;
-  const int per = (n_blocks + want - 1) / want;
+  const int want = (256 + wgs - 1) / wgs;
+  int per = (n_blocks + want - 1) / want;
+  if (per < 2) per = 2;
+  if ((n_blocks + per - 1) / per > 32) per = (n_blocks + 31) / 32;  // combine handles <= 32 splits
+  if (per > n_blocks) per = n_blocks;
   *bps = per;
   return (n_blocks + per - 1) / per;
 }
@@ -148,6 +149,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
     return cerr(UAD_E_UNSUPPORTED, "uad_create: head_dim must be 64, 128 or 256");
   if (m.n_heads % m.n_kv_heads) return cerr(UAD_E_UNSUPPORTED, "uad_create: n_kv_heads must divide n_heads");
   if (m.action_dim > 64) return cerr(UAD_E_UNSUPPORTED, "uad_create: action_dim must be <= 64");
+  if (m.d_model > 2048) return cerr(UAD_E_UNSUPPORTED, "uad_create: d_model must be <= 2048");
 
   hipError_t e = hipSetDevice(device);
   if (e != hipSuccess) return cerr(UAD_E_HIP, std::string("hipSetDevice: ") + hipGetErrorString(e));
@@ -263,11 +265,12 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->attn_part_elems = part;
   const size_t M = c->m_alloc;
   Carve a;
-  // GEMM inputs (te, z, n, o, g) hold two bf16 planes (hi, lo) of M rows each
+  // GEMM inputs (te, z, n, o, g) hold two bf16 planes (hi, lo) of M rows each;
+  // part holds the K-split partial sums of the projections that feed the residual stream
   size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(2 * M * 2 * d), o_z = a.take<uint16_t>(2 * M * d),
          o_n = a.take<uint16_t>(2 * M * d), o_o = a.take<uint16_t>(2 * M * c->q_dim), o_g = a.take<uint16_t>(2 * M * F),
          o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
-         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2);
+         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_part = a.take<float>((size_t)kMaxSplits * M * d);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -284,6 +287,12 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->q = (__bf16 *)(ab + o_q);
   c->attn_opart = (float *)(ab + o_op);
   c->attn_ml = (float *)(ab + o_ml);
+  c->part = (float *)(ab + o_part);
+  e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
+  if (e != hipSuccess) {
+    uad_destroy(c);
+    return cerr(UAD_E_HIP, std::string("hipStreamCreate(capture): ") + hipGetErrorString(e));
+  }
   *out = c;
   g_create_err.clear();
   return UAD_OK;
@@ -302,6 +311,8 @@ void uad_destroy(uad_ctx *c) {
     (void)hipEventDestroy(r.b);
   }
   for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
+  for (auto &ge : c->graphs) (void)hipGraphExecDestroy(ge.exec);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
 }
@@ -497,40 +508,48 @@ static uad_status check_step_args(uad_ctx *c, const void *x, const void *t, cons
   return UAD_OK;
 }
 
-// Enqueue one joint step: F_theta over all B*H tokens, then the masked Euler update.
-static uad_status enqueue_step(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
-                               const uint8_t *next_mask, int is_last, int step, float *v_out, float *released,
-                               int32_t *release_step, int B, int H) {
-  const int M = B * H, d = c->d;
-  hipStream_t s = c->stream;
+// Enqueue one joint step on stream s: F_theta over all B*H tokens, then the
+// masked Euler update.  Kernel sequence: temb -> time-MLP in -> time-MLP out
+// (K-split partials) -> reduce (+RMSNorm) -> per layer [QKV -> attention ->
+// O (partials) -> reduce (+RMSNorm) -> gate/up GeGLU -> down (partials) ->
+// reduce (+RMSNorm of the next layer)] -> final norm/projection/Euler.
+static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float *t, const float *dt,
+                               const uint8_t *mask, const uint8_t *next_mask, int is_last, int step, float *v_out,
+                               float *released, int32_t *release_step, int B, int H) {
+  const int M = B * H, d = c->d, F = c->F;
+  const size_t MA = c->m_alloc;
   hipError_t e = hipSuccess;
+  // measurement hook: the launch records a start/stop event pair taken from
+  // the kernel's own dispatch packet (ea_/eb_ are nullptr when not profiling)
 #define UAD_CHECK_CLS(cls, call)                       \
   do {                                                 \
     hipEvent_t ea_ = nullptr, eb_ = nullptr;           \
     if (c->prof_on) {                                  \
       ea_ = pool_event(c);                             \
       eb_ = pool_event(c);                             \
-      (void)hipEventRecord(ea_, s);                    \
     }                                                  \
     e = (call);                                        \
     if (e != hipSuccess) return hip_fail(c, e, #call); \
-    if (c->prof_on) {                                  \
-      (void)hipEventRecord(eb_, s);                    \
-      c->prof_pending.push_back({cls, ea_, eb_});      \
-    }                                                  \
+    if (c->prof_on) c->prof_pending.push_back({cls, ea_, eb_}); \
   } while (0)
   if (!c->dbg) {
-    const size_t MA = c->m_alloc;
     UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
-                                      MA * 2 * d, s));
+                                      MA * 2 * d, s, ea_, eb_));
     GemmArgs g{};
     g.M = M;
-    g.A = c->a_te; g.lda = 2 * d; g.a_plane = MA * 2 * d; g.W = c->t1_w; g.N = d; g.K = 2 * d;
+    g.A = c->a_te; g.a_plane = MA * 2 * d; g.W = c->t1_w; g.N = d; g.K = 2 * d;
     g.out = c->a_z; g.ldo = d; g.out_plane = MA * d; g.bias = c->t1_b;
-    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU_BF16, g, s));
-    g.A = c->a_z; g.lda = d; g.a_plane = MA * d; g.W = c->t2_w; g.N = d; g.K = d;
-    g.out = c->h; g.ldo = d; g.out_plane = 0; g.bias = c->t2_b;
-    UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_F32, g, s));
+    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU_BF16, g, plan_gemm(EPI_BIAS_SILU_BF16, M, d, 2 * d,
+                                                                              kMaxSplits), s, ea_, eb_));
+    GemmArgs g2{};
+    g2.M = M; g2.A = c->a_z; g2.a_plane = MA * d; g2.W = c->t2_w; g2.N = d; g2.K = d;
+    g2.out = c->part; g2.ldo = d; g2.part_rows = (int)MA;
+    const GemmPlan p2 = plan_gemm(EPI_PARTIAL_F32, M, d, d, kMaxSplits);
+    UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_PARTIAL_F32, g2, p2, s, ea_, eb_));
+    ReduceArgs r{};
+    r.h = c->h; r.part = c->part; r.splits = p2.splits; r.part_rows = (int)MA; r.M = M; r.d = d;
+    r.bias = c->t2_b; r.gain = c->layers[0].attn_norm; r.eps = c->cfg.rms_eps; r.n = c->a_n; r.n_plane = MA * d;
+    UAD_CHECK_CLS(K_REDUCE, launch_reduce(r, s, ea_, eb_));
 
     AttnArgs at{};
     at.q = c->q; at.ldq = c->q_dim; at.s_alloc = c->s_alloc; at.n_keys = c->prefix_len + H;
@@ -540,29 +559,37 @@ static uad_status enqueue_step(uad_ctx *c, float *x, const float *t, const float
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
     at.o = c->a_o; at.ldo = c->q_dim; at.o_plane = MA * c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
 
+    const GemmPlan pq = plan_gemm(EPI_QKV, M, c->n_qkv, d, kMaxSplits);
+    const GemmPlan po = plan_gemm(EPI_PARTIAL_F32, M, d, c->q_dim, kMaxSplits);
+    const GemmPlan pg = plan_gemm(EPI_GEGLU_BF16, M, 2 * F, d, kMaxSplits);
+    const GemmPlan pd = plan_gemm(EPI_PARTIAL_F32, M, d, F, kMaxSplits);
     for (int l = 0; l < c->L; ++l) {
       const uad_layer_ptrs &lp = c->layers[l];
       __bf16 *kc = c->kcache + l * c->kv_layer_elems;
       __bf16 *vtc = c->vtcache + l * c->kv_layer_elems;
-      UAD_CHECK_CLS(K_RMSNORM, launch_rmsnorm(c->h, lp.attn_norm, c->cfg.rms_eps, M, d, c->a_n, MA * d, s));
       GemmArgs q{};
-      q.M = M; q.A = c->a_n; q.lda = d; q.a_plane = MA * d; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
+      q.M = M; q.A = c->a_n; q.a_plane = MA * d; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
-      UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, s));
+      UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, pq, s, ea_, eb_));
       at.kc = kc; at.vtc = vtc;
-      UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s));
+      UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s, ea_, eb_));
       GemmArgs o{};
-      o.M = M; o.A = c->a_o; o.lda = c->q_dim; o.a_plane = MA * c->q_dim; o.W = lp.wo; o.N = d; o.K = c->q_dim; o.out = c->h; o.ldo = d;
-      UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, s));
-      UAD_CHECK_CLS(K_RMSNORM, launch_rmsnorm(c->h, lp.mlp_norm, c->cfg.rms_eps, M, d, c->a_n, MA * d, s));
+      o.M = M; o.A = c->a_o; o.a_plane = MA * c->q_dim; o.W = lp.wo; o.N = d; o.K = c->q_dim;
+      o.out = c->part; o.ldo = d; o.part_rows = (int)MA;
+      UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_PARTIAL_F32, o, po, s, ea_, eb_));
+      r.bias = nullptr; r.splits = po.splits; r.gain = lp.mlp_norm;
+      UAD_CHECK_CLS(K_REDUCE, launch_reduce(r, s, ea_, eb_));
       GemmArgs gu{};
-      gu.M = M; gu.A = c->a_n; gu.lda = d; gu.a_plane = MA * d; gu.W = lp.wgu; gu.N = 2 * c->F; gu.K = d;
-      gu.out = c->a_g; gu.ldo = c->F; gu.out_plane = MA * c->F;
-      UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU_BF16, gu, s));
+      gu.M = M; gu.A = c->a_n; gu.a_plane = MA * d; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
+      gu.out = c->a_g; gu.ldo = F; gu.out_plane = MA * F;
+      UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU_BF16, gu, pg, s, ea_, eb_));
       GemmArgs dn{};
-      dn.M = M; dn.A = c->a_g; dn.lda = c->F; dn.a_plane = MA * c->F; dn.W = lp.wdown; dn.N = d; dn.K = c->F; dn.out = c->h; dn.ldo = d;
-      UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_RESID_F32, dn, s));
+      dn.M = M; dn.A = c->a_g; dn.a_plane = MA * F; dn.W = lp.wdown; dn.N = d; dn.K = F;
+      dn.out = c->part; dn.ldo = d; dn.part_rows = (int)MA;
+      UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_PARTIAL_F32, dn, pd, s, ea_, eb_));
+      r.splits = pd.splits; r.gain = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr;
+      UAD_CHECK_CLS(K_REDUCE, launch_reduce(r, s, ea_, eb_));
     }
   }
   FinalArgs f{};
@@ -570,8 +597,79 @@ static uad_status enqueue_step(uad_ctx *c, float *x, const float *t, const float
   f.M = M; f.d = d; f.Da = c->Da; f.x = x; f.t = t; f.dt = dt; f.mask = mask; f.next_mask = next_mask;
   f.is_last_step = is_last; f.step = step; f.v_out = v_out; f.released = released; f.release_step = release_step;
   f.debug_field = c->dbg ? 1 : 0; f.dbg_alpha = c->dbg_alpha; f.dbg_beta = c->dbg_beta;
-  UAD_CHECK_CLS(K_FINAL, launch_final(f, s));
+  UAD_CHECK_CLS(K_FINAL, launch_final(f, s, ea_, eb_));
 #undef UAD_CHECK_CLS
+  return UAD_OK;
+}
+
+// Enqueue a whole schedule (or one step when t etc. are single slices) on s.
+static uad_status enqueue_schedule(uad_ctx *c, hipStream_t s, const GraphKey &k) {
+  const size_t M = (size_t)k.B * k.H;
+  if (k.step_ticks) {
+    hipError_t e = launch_stamp(k.step_ticks, s);
+    if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
+  }
+  for (int st = 0; st < k.n_steps; ++st) {
+    const bool last = k.is_schedule ? st == k.n_steps - 1 : false;
+    const uint8_t *next = (k.is_schedule && !last) ? k.mask + (st + 1) * M : nullptr;
+    uad_status rs = enqueue_step(c, s, k.x, k.t + st * M, k.dt + st * M, k.mask + st * M, next, last ? 1 : 0, st,
+                                 k.v_out, k.released, k.release_step, k.B, k.H);
+    if (rs != UAD_OK) return rs;
+    if (k.step_ticks) {
+      hipError_t e = launch_stamp(k.step_ticks + st + 1, s);
+      if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
+    }
+  }
+  return UAD_OK;
+}
+
+// Run the work described by k: replay a cached hipGraph of it when possible
+// (one graph launch for the whole schedule), else capture one; direct launches
+// while profiling or in the synthetic-velocity test mode.
+static uad_status run_work(uad_ctx *c, GraphKey k) {
+  k.prefix_len = c->prefix_len;
+  k.prefix_batch = c->prefix_batch;
+  // the measurement hook and the synthetic-velocity test mode launch directly
+  if (c->dbg || c->graph_broken || c->prof_on) return enqueue_schedule(c, c->stream, k);
+  ++c->graph_clock;
+  uad_ctx::GraphEntry *hit = nullptr;
+  for (auto &ge : c->graphs)
+    if (ge.key == k) hit = &ge;
+  if (!hit) {
+    hipError_t e = hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      c->graph_broken = true;
+      return enqueue_schedule(c, c->stream, k);
+    }
+    uad_status rs = enqueue_schedule(c, c->cap_stream, k);
+    hipGraph_t graph = nullptr;
+    e = hipStreamEndCapture(c->cap_stream, &graph);
+    if (rs != UAD_OK) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return rs;
+    }
+    hipGraphExec_t exec = nullptr;
+    if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    if (graph) (void)hipGraphDestroy(graph);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      c->graph_broken = true;
+      return enqueue_schedule(c, c->stream, k);
+    }
+    if (c->graphs.size() >= 8) {  // evict the least recently used graph
+      size_t lru = 0;
+      for (size_t i = 1; i < c->graphs.size(); ++i)
+        if (c->graphs[i].last_use < c->graphs[lru].last_use) lru = i;
+      (void)hipGraphExecDestroy(c->graphs[lru].exec);
+      c->graphs.erase(c->graphs.begin() + lru);
+    }
+    c->graphs.push_back({k, exec, c->graph_clock});
+    hit = &c->graphs.back();
+  }
+  hit->last_use = c->graph_clock;
+  hipError_t e = hipGraphLaunch(hit->exec, c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "hipGraphLaunch");
   return UAD_OK;
 }
 
@@ -581,7 +679,10 @@ uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *d
   uad_status st = check_step_args(c, x, t, dt, mask, batch, chunk, "uad_denoise_step");
   if (st != UAD_OK) return st;
   (void)hipSetDevice(c->device);
-  return enqueue_step(c, x, t, dt, mask, nullptr, 0, 0, v_out, nullptr, nullptr, batch, chunk);
+  GraphKey k{};
+  k.is_schedule = false;
+  k.x = x; k.t = t; k.dt = dt; k.mask = mask; k.v_out = v_out; k.n_steps = 1; k.B = batch; k.H = chunk;
+  return run_work(c, k);
 }
 
 uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, const float *dt_sched,
@@ -592,23 +693,11 @@ uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, cons
   if (st != UAD_OK) return st;
   if (n_steps < 1) return fail(c, UAD_E_INVALID, "uad_denoise_schedule: n_steps must be >= 1");
   (void)hipSetDevice(c->device);
-  const size_t M = (size_t)batch * chunk;
-  if (step_ticks) {
-    hipError_t e = launch_stamp(step_ticks, c->stream);
-    if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
-  }
-  for (int k = 0; k < n_steps; ++k) {
-    const bool last = k == n_steps - 1;
-    st = enqueue_step(c, x, t_sched + k * M, dt_sched + k * M, mask_sched + k * M,
-                      last ? nullptr : mask_sched + (k + 1) * M, last ? 1 : 0, k, nullptr, released, release_step,
-                      batch, chunk);
-    if (st != UAD_OK) return st;
-    if (step_ticks) {
-      hipError_t e = launch_stamp(step_ticks + k + 1, c->stream);
-      if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
-    }
-  }
-  return UAD_OK;
+  GraphKey k{};
+  k.is_schedule = true;
+  k.x = x; k.t = t_sched; k.dt = dt_sched; k.mask = mask_sched; k.n_steps = n_steps; k.B = batch; k.H = chunk;
+  k.released = released; k.release_step = release_step; k.step_ticks = step_ticks;
+  return run_work(c, k);
 }
 
 uad_status uad_synchronize(uad_ctx *c) {

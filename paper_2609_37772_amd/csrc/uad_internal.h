@@ -2,6 +2,7 @@
 // Not part of the public ABI (see include/uad.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -12,6 +13,16 @@
 #include "../../include/uad.h"
 
 namespace uad {
+
+// Kernel launch; with events (measurement hook) the start/stop timestamps are
+// taken from the dispatch packet itself, so they time exactly the kernel.
+#define UAD_LAUNCH(kernel, grid, block, shmem, stream, ev0, ev1, ...)                                  \
+  do {                                                                                               \
+    if ((ev0) || (ev1))                                                                              \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev0, ev1, 0, __VA_ARGS__);           \
+    else                                                                                             \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                           \
+  } while (0)
 
 // ---------------------------------------------------------------------------
 // Vector types for the gfx950 bf16 MFMA builtins
@@ -40,26 +51,43 @@ __device__ __forceinline__ void store_split(__bf16 *hi, size_t plane, float v) {
   hi[plane] = (__bf16)(v - (float)h);
 }
 
+// Activation operands use the same fragment order as the weights: a
+// [rows][K] matrix (rows padded to 16) is stored as [rows/16][K/32][64][8],
+// element (r, c) at lane (r & 15) + 16 * ((c & 31) >> 3), slot c & 7, so a
+// wave loads one 16x32 A fragment as 1 KiB contiguous.
+__host__ __device__ __forceinline__ size_t afrag_index(int r, int c, int KB) {
+  return ((size_t)((r >> 4) * KB + (c >> 5)) * 64 + (r & 15) + 16 * ((c & 31) >> 3)) * 8 + (c & 7);
+}
+
 // ---------------------------------------------------------------------------
 // Kernel argument blocks
 // ---------------------------------------------------------------------------
 enum Epilogue : int {
-  EPI_BIAS_SILU_BF16 = 0,  // out bf16 = silu(acc + bias)
-  EPI_BIAS_F32 = 1,        // out fp32 = acc + bias
-  EPI_RESID_F32 = 2,       // out fp32 += acc
-  EPI_GEGLU_BF16 = 3,      // out bf16 = gelu_tanh(acc_gate) * acc_up (tile-interleaved gate/up)
+  EPI_BIAS_SILU_BF16 = 0,  // out = split bf16 planes of silu(acc + bias), fragment order
+  EPI_PARTIAL_F32 = 1,     // out[split][row][col] = fp32 partial sum over this K split
+  EPI_GEGLU_BF16 = 3,      // out = split planes of gelu_tanh(acc_gate) * acc_up (tile-interleaved gate/up)
   EPI_QKV = 4,             // q -> bf16 q buffer; k, v -> per-layer K / V^T store
 };
 
+struct GemmPlan {
+  int T;       // 16-column weight tiles per workgroup
+  int splits;  // K splits (grid.y)
+  int kpw;     // 32-deep k-blocks per wave and pass
+  int waves;   // waves per workgroup
+  int passes;  // runs of kpw blocks per wave
+  bool ok;
+};
+
 struct GemmArgs {
-  const __bf16 *A;  // activations, hi plane [>= round_up(M,64)][lda] bf16
+  const __bf16 *A;  // activations, hi plane, fragment order [rows/16][K/32][64][8]
   int lda;
   size_t a_plane;   // element offset of the lo plane
   size_t out_plane; // element offset of the lo plane of a split bf16 output
+  int part_rows;    // row stride between K-split partials (EPI_PARTIAL_F32)
   const __bf16 *W;  // packed weights, N/16 tiles x K/32 blocks
   int M, N, K;      // N counts packed output columns (2F for gate/up)
   void *out;        // epilogue destination
-  int ldo;
+  int ldo;          // its row length (= K of the consuming GEMM for fragment-order outputs)
   const float *bias;
   // EPI_QKV destinations
   __bf16 *kc;   // layer K store [B][Hkv][S_alloc][hd]
@@ -82,6 +110,19 @@ struct AttnArgs {
   size_t o_plane;
   float *opart;      // [splits][B*Hkv][rows_pad][hd] (splits > 1)
   float *mlpart;     // [splits][B*Hkv][rows_pad][2]
+};
+
+// h = (bias or h) + sum of K-split partials (fixed order); optionally the next
+// GEMM's operand n = split planes of RMSNorm(h) * gain, in fragment order.
+struct ReduceArgs {
+  float *h;            // [M][d]
+  const float *part;   // [splits][part_rows][d]
+  int splits, part_rows, M, d;
+  const float *bias;   // non-null: h = bias + sum (initialisation)
+  const float *gain;   // non-null: write n
+  float eps;
+  __bf16 *n;
+  size_t n_plane;
 };
 
 struct FinalArgs {
@@ -107,13 +148,18 @@ struct FinalArgs {
 // ---------------------------------------------------------------------------
 // Launchers (defined in the .hip translation units)
 // ---------------------------------------------------------------------------
-hipError_t launch_gemm(int epi, const GemmArgs &g, hipStream_t s);
-hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s);
+GemmPlan plan_gemm(int epi, int M, int N, int K, int max_splits);
+// ev0 / ev1: optional events recorded at the start / end of the launched
+// kernel(s) (nullptr for none).
+hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_t s, hipEvent_t ev0 = nullptr,
+                       hipEvent_t ev1 = nullptr);
+hipError_t launch_reduce(const ReduceArgs &r, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0 = nullptr,
+                            hipEvent_t ev1 = nullptr);
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
-                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s);
-hipError_t launch_rmsnorm(const float *h, const float *gain, float eps, int M, int d, __bf16 *out,
-                          size_t plane, hipStream_t s);
-hipError_t launch_final(const FinalArgs &f, hipStream_t s);
+                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s,
+                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
 
 // Host-side helpers (schedule.cpp)
@@ -125,6 +171,24 @@ bool build_schedule_host(const int32_t *budgets, int batch, int chunk, int max_s
 // ---------------------------------------------------------------------------
 // Context
 // ---------------------------------------------------------------------------
+// Everything a captured step/schedule graph depends on.
+struct GraphKey {
+  bool is_schedule;
+  float *x;
+  const float *t, *dt;
+  const uint8_t *mask;
+  float *v_out, *released;
+  int32_t *release_step;
+  uint64_t *step_ticks;
+  int n_steps, B, H, prefix_len, prefix_batch;
+  bool operator==(const GraphKey &o) const {
+    return is_schedule == o.is_schedule && x == o.x && t == o.t && dt == o.dt && mask == o.mask &&
+           v_out == o.v_out && released == o.released && release_step == o.release_step &&
+           step_ticks == o.step_ticks && n_steps == o.n_steps && B == o.B && H == o.H &&
+           prefix_len == o.prefix_len && prefix_batch == o.prefix_batch;
+  }
+};
+
 struct uad_layer_ptrs {
   const __bf16 *wqkv, *wo, *wgu, *wdown;
   const float *attn_norm, *mlp_norm;
@@ -162,7 +226,19 @@ struct uad_ctx {
   __bf16 *a_te = nullptr, *a_z = nullptr, *a_n = nullptr, *a_o = nullptr, *a_g = nullptr, *q = nullptr;
   float *attn_opart = nullptr, *attn_ml = nullptr;
   size_t attn_part_elems = 0;
+  float *part = nullptr;  // K-split partials [splits][m_alloc][d]
   void *abuf = nullptr;
+
+  // captured step / schedule graphs (small LRU cache)
+  struct GraphEntry {
+    GraphKey key;
+    hipGraphExec_t exec;
+    uint64_t last_use;
+  };
+  std::vector<GraphEntry> graphs;
+  uint64_t graph_clock = 0;
+  hipStream_t cap_stream = nullptr;
+  bool graph_broken = false;
 
   // measurement hook: events around every launch, grouped by kernel class
   struct ProfRec {
