@@ -4,20 +4,26 @@
 //
 // Shape of the work: M is the token count (B*H: 16..3200), N and K are the
 // projection sizes (256..8192).  At batch 1 a step streams ~0.6 GB of weights
-// for ~50 tokens, so the kernel is organised around the weight stream:
-//   * a workgroup owns T 16-column weight tiles, one 64-row block and one
-//     K split; its waves cut that K range into runs of KPW 32-deep blocks and
-//     issue all loads of a run (weights and activations) before its first
-//     MFMA, so each wave keeps KPW*(T + 2*4) 16-byte loads in flight;
+// for ~50 tokens, and each CU's vector-memory pipe (not HBM) is what a
+// workgroup waits on, so the work is cut to balance the bytes per workgroup:
+//   * a workgroup owns T 16-column weight tiles over the full K and a group of
+//     up to four 16-row tiles (batch 1: the ~50 rows are split over 2-3
+//     workgroups, which re-read the weight tile from L2 instead of every
+//     workgroup reading all rows of the activations);
+//   * its waves cut K into runs of KPW 32-deep blocks and issue all loads of
+//     a run (weights and activations) before its first MFMA;
 //   * weights and activations are both stored in MFMA fragment order, so each
-//     operand load is one aligned 16-byte load per lane and 1 KiB contiguous
-//     per wave;
+//     operand load is one aligned 16-byte load per lane, 1 KiB per wave;
 //   * activations are hi/lo bf16 planes: every weight fragment feeds two
 //     MFMAs (the MFMA units idle at batch 1, HBM does not);
-//   * rows past M are neither loaded nor multiplied;
 //   * per-wave partial tiles are reduced through LDS in fixed wave order
-//     (deterministic, no atomics); with a K split the workgroup writes an fp32
-//     partial and a separate reduce kernel sums the splits in fixed order.
+//     (deterministic, no atomics).
+// RMSNorm is folded into the GEMMs: the residual GEMMs (time-MLP out, O, down)
+// update h for their columns, write the per-16-column sum of squares of every
+// row and the next operand split(h * gain_next); the GEMMs that consume a
+// normalised input (QKV, gate/up) scale their accumulators by
+// rstd[row] = (sum of those sums / d + eps)^-1/2, since
+// RMSNorm(h) W^T = rstd * ((h * gain) W^T).
 #include "uad_internal.h"
 
 namespace uad {
@@ -29,38 +35,63 @@ __device__ __forceinline__ float gelu_tanh(float z) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
+constexpr int kMaxTilesPerGroup = 4;
+
 template <int EPI, int T, int KPW>
 __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   extern __shared__ float red[];  // [waves][4*T*4 slots][64 lanes]
+  __shared__ float rpart[8][64];  // partial sums of ssq for rstd
+  __shared__ float rstd_s[64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int waves = blockDim.x >> 6;
   const int tile0 = blockIdx.x * T;  // first 16-column weight tile
-  const int split = blockIdx.y;
-  const int m0 = blockIdx.z * 64;
+  const int MT = (g.M + 15) >> 4;
+  const int mt0 = (blockIdx.z * MT) / gridDim.z;
+  const int nmt = ((blockIdx.z + 1) * MT) / gridDim.z - mt0;  // 1..4, uniform
+  const int m0 = mt0 * 16;
   const int KB = g.K / kTileK;
-  const int kb_split = KB / gridDim.y;
-  const int passes = kb_split / (KPW * waves);
-  const int mt_valid = min(4, (g.M - m0 + 15) >> 4);  // wave-uniform
+  const int passes = KB / (KPW * waves);
 
-  f32x4 acc[4][T];
+  // rstd of this group's rows, from the residual GEMM's per-tile sums of
+  // squares (fixed summation order); loads issued before the operand loads
+  // (the first 16 tiles of each wave are unconditional loads with clamped
+  // indices so they issue back to back; d/16 tiles need more only when fewer
+  // than d/256 waves run)
+  if ((EPI == EPI_QKV || EPI == EPI_GEGLU_BF16) && g.use_rstd) {
+    const int row = min(m0 + lane, g.M - 1);
+    float vals[16];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+    for (int i = 0; i < 16; ++i) {
+      const int j = wave + i * waves;
+      const float val = g.ssq[(size_t)min(j, g.ssq_tiles - 1) * g.m_alloc + row];
+      vals[i] = j < g.ssq_tiles ? val : 0.f;
+    }
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc += vals[i];
+    for (int j = wave + 16 * waves; j < g.ssq_tiles; j += waves) acc += g.ssq[(size_t)j * g.m_alloc + row];
+    rpart[wave][lane] = acc;
+  }
+
+  f32x4 acc[kMaxTilesPerGroup][T];
+#pragma unroll
+  for (int mt = 0; mt < kMaxTilesPerGroup; ++mt)
 #pragma unroll
     for (int t = 0; t < T; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int pass = 0; pass < passes; ++pass) {
-    const int kb0 = split * kb_split + (pass * waves + wave) * KPW;
-    bf16x8 w[KPW][T], ah[KPW][4], al[KPW][4];
+    const int kb0 = (pass * waves + wave) * KPW;
+    bf16x8 w[KPW][T], ah[KPW][kMaxTilesPerGroup], al[KPW][kMaxTilesPerGroup];
     const __bf16 *wp = g.W + ((size_t)tile0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
     for (int j = 0; j < KPW; ++j)
 #pragma unroll
       for (int t = 0; t < T; ++t) w[j][t] = *(const bf16x8 *)(wp + ((size_t)t * KB + j) * kBlockElems);
-    const __bf16 *ap = g.A + ((size_t)(m0 >> 4) * KB + kb0) * kBlockElems + lane * 8;
+    const __bf16 *ap = g.A + ((size_t)mt0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      const bool ok = mt < mt_valid && (m0 + mt * 16 + (lane & 15)) < g.M;
+    for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
+      const bool ok = mt < nmt && (m0 + mt * 16 + (lane & 15)) < g.M;
 #pragma unroll
       for (int j = 0; j < KPW; ++j) {
         if (ok) {
@@ -74,8 +105,8 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       }
     }
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      if (mt >= mt_valid) break;
+    for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
+      if (mt >= nmt) break;
 #pragma unroll
       for (int j = 0; j < KPW; ++j)
 #pragma unroll
@@ -87,23 +118,33 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   }
 
   // Cross-wave reduction through LDS, fixed order over waves.
-  constexpr int SLOTS = 16 * T;  // (mt, t, r) triples per lane
+  constexpr int SLOTS = kMaxTilesPerGroup * T * 4;  // (mt, t, r) triples per lane
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < kMaxTilesPerGroup; ++mt)
 #pragma unroll
     for (int t = 0; t < T; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[((wave * SLOTS) + (mt * T + t) * 4 + r) * 64 + lane] = acc[mt][t][r];
   __syncthreads();
+  if ((EPI == EPI_QKV || EPI == EPI_GEGLU_BF16) && g.use_rstd && threadIdx.x < 64) {
+    float ss = 0.f;
+    for (int w2 = 0; w2 < waves; ++w2) ss += rpart[w2][threadIdx.x];
+    rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
+  }
+  __syncthreads();
 
-  // element e = slot*64 + lane, slot = (mt*T + t)*4 + r; the D fragment of a
-  // 16x16 MFMA holds row 4*(lane>>4)+r, column lane&15 in each lane.
-  const int n_out = (EPI == EPI_GEGLU_BF16) ? 1024 * (T / 2) : 1024 * T;
-  for (int e = threadIdx.x; e < n_out; e += blockDim.x) {
+  // Epilogue. Element e = slot*64 + lane with slot = (mt*T + t)*4 + r (for
+  // GeGLU slot = (mt*(T/2) + pair)*4 + r); the D fragment of a 16x16 MFMA holds
+  // row 4*(lane>>4)+r, column lane&15.  The per-wave trip count is uniform and
+  // the 16 lanes holding one row are always active together.
+  const int n_out = (EPI == EPI_GEGLU_BF16) ? nmt * 256 * (T / 2) : nmt * 256 * T;
+  for (int e0 = 0; e0 < n_out; e0 += blockDim.x) {
+    const int e = e0 + threadIdx.x;
+    if (e >= n_out) continue;  // whole waves only (n_out and blockDim are multiples of 64)
     const int ln = e & 63;
     const int slot = e >> 6;
     int mt, t, r;
-    if (EPI == EPI_GEGLU_BF16) {  // slot = (mt*(T/2) + pair)*4 + r; gate tile 2*pair, up tile 2*pair+1
+    if (EPI == EPI_GEGLU_BF16) {
       r = slot & 3;
       const int q = slot >> 2;
       t = 2 * (q % (T / 2));
@@ -113,24 +154,45 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       t = (slot >> 2) % T;
       mt = (slot >> 2) / T;
     }
-    const int row = m0 + mt * 16 + (ln >> 4) * 4 + r;
-    if (row >= g.M) continue;
+    const int rl = mt * 16 + (ln >> 4) * 4 + r;  // row within the group
+    const int row = m0 + rl;
+    const bool row_ok = row < g.M;
     const int s0 = (mt * T + t) * 4 + r;
     float v = 0.f;
     for (int w2 = 0; w2 < waves; ++w2) v += red[(w2 * SLOTS + s0) * 64 + ln];
+    if (EPI == EPI_RESID_F32) {
+      const int col = (tile0 + t) * 16 + (ln & 15);
+      float hv = 0.f;
+      if (row_ok) {
+        float *hp = (float *)g.out + (size_t)row * g.ldo + col;
+        hv = (g.bias ? g.bias[col] : *hp) + v;
+        *hp = hv;
+      }
+      float sq = hv * hv;  // sum over the 16 columns of this row (lanes sharing ln>>4)
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
+      if (row_ok) {
+        if ((ln & 15) == 0) g.ssq[(size_t)(tile0 + t) * g.m_alloc + row] = sq;
+        if (g.gain_next)
+          store_split(g.next + afrag_index(row, col, g.N / kTileK), g.next_plane, hv * g.gain_next[col]);
+      }
+      continue;
+    }
+    if (!row_ok) continue;
+    const float rs = ((EPI == EPI_QKV || EPI == EPI_GEGLU_BF16) && g.use_rstd) ? rstd_s[rl] : 1.0f;
     if (EPI == EPI_GEGLU_BF16) {
       const int s1 = (mt * T + t + 1) * 4 + r;
       float u = 0.f;
       for (int w2 = 0; w2 < waves; ++w2) u += red[(w2 * SLOTS + s1) * 64 + ln];
       const int col = ((tile0 + t) >> 1) * 16 + (ln & 15);
-      store_split((__bf16 *)g.out + afrag_index(row, col, g.ldo / kTileK), g.out_plane, gelu_tanh(v) * u);
+      store_split((__bf16 *)g.out + afrag_index(row, col, g.ldo / kTileK), g.out_plane,
+                  gelu_tanh(v * rs) * (u * rs));
     } else {
       const int col = (tile0 + t) * 16 + (ln & 15);
       if (EPI == EPI_BIAS_SILU_BF16) {
         store_split((__bf16 *)g.out + afrag_index(row, col, g.ldo / kTileK), g.out_plane, silu(v + g.bias[col]));
-      } else if (EPI == EPI_PARTIAL_F32) {
-        ((float *)g.out)[((size_t)split * g.part_rows + row) * g.ldo + col] = v;
       } else if (EPI == EPI_QKV) {
+        v *= rs;
         if (col < g.q_dim) {
           ((__bf16 *)g.out)[(size_t)row * g.ldo + col] = (__bf16)v;
         } else {
@@ -154,32 +216,40 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 
 template <int EPI, int T, int KPW>
 static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  dim3 grid(g.N / kTileN / T, p.splits, (g.M + 63) / 64);
-  const uint32_t lds = (uint32_t)(p.waves * 16 * T * 64 * sizeof(float));
+  dim3 grid(g.N / kTileN / T, 1, p.mgroups);
+  const uint32_t lds = (uint32_t)(p.waves * kMaxTilesPerGroup * T * 4 * 64 * sizeof(float));
   UAD_LAUNCH((gemm_kernel<EPI, T, KPW>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
 
-// Launch shape: T tiles per workgroup (2 = a gate/up pair), a power-of-two K
-// split (partial-output GEMMs only) until the grid has >= 256 workgroups while
-// each split keeps >= 4 k-blocks, KPW = 4 k-blocks per wave and pass, <= 8
-// waves, and as many passes as the split's K range needs.
-GemmPlan plan_gemm(int epi, int M, int N, int K, int max_splits) {
+// Launch shape.  Row groups: up to four 16-row tiles each; when the rows fit
+// in four tiles they are spread over more groups until the grid has about 256
+// workgroups (a last tile with fewer than 8 valid rows stays with the previous
+// group).  K: runs of KPW = 4 k-blocks per wave, <= 8 waves, as many passes as
+// needed.
+GemmPlan plan_gemm(int epi, int M, int N, int K) {
   GemmPlan p{};
   const int KB = K / kTileK;
   p.T = (epi == EPI_GEGLU_BF16) ? 2 : 1;
-  const int groups = (N / kTileN / p.T) * ((M + 63) / 64);
-  p.splits = 1;
-  if (epi == EPI_PARTIAL_F32)
-    while (p.splits * 2 <= max_splits && groups * p.splits < 256 && KB % (p.splits * 2) == 0 &&
-           KB / (p.splits * 2) >= 4)
-      p.splits *= 2;
-  const int kb_split = KB / p.splits;
-  p.kpw = (kb_split % 4 == 0) ? 4 : (kb_split % 2 == 0 ? 2 : 1);
-  p.waves = kb_split / p.kpw < 8 ? kb_split / p.kpw : 8;
-  while (p.waves > 1 && kb_split % (p.kpw * p.waves) != 0) --p.waves;
-  p.passes = kb_split / (p.kpw * p.waves);
-  p.ok = KB >= 1 && N % (kTileN * p.T) == 0 && p.waves >= 1 && kb_split == p.passes * p.kpw * p.waves;
+  const int ngroups = N / kTileN / p.T;
+  const int MT = (M + 15) / 16;
+  if (MT > kMaxTilesPerGroup) {
+    p.mgroups = (MT + kMaxTilesPerGroup - 1) / kMaxTilesPerGroup;
+  } else {
+    int mt_eff = MT;
+    if (MT > 1 && M - (MT - 1) * 16 < 8) mt_eff = MT - 1;
+    int want = (256 + ngroups - 1) / ngroups;
+    p.mgroups = want < mt_eff ? want : mt_eff;
+    if (p.mgroups < 1) p.mgroups = 1;
+  }
+  p.kpw = (KB % 4 == 0) ? 4 : (KB % 2 == 0 ? 2 : 1);
+  p.waves = KB / p.kpw < 8 ? KB / p.kpw : 8;
+  while (p.waves > 1 && KB % (p.kpw * p.waves) != 0) --p.waves;
+  p.passes = KB / (p.kpw * p.waves);
+  // every row group must hold 1..4 tiles
+  const int max_tiles = (MT + p.mgroups - 1) / p.mgroups;
+  p.ok = KB >= 1 && N % (kTileN * p.T) == 0 && p.waves >= 1 && KB == p.passes * p.kpw * p.waves &&
+         max_tiles <= kMaxTilesPerGroup && p.mgroups <= MT;
   return p;
 }
 
@@ -196,7 +266,7 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
   if (!p.ok) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_BIAS_SILU_BF16: UAD_GEMM_KPW_CASES(EPI_BIAS_SILU_BF16, 1)
-    case EPI_PARTIAL_F32: UAD_GEMM_KPW_CASES(EPI_PARTIAL_F32, 1)
+    case EPI_RESID_F32: UAD_GEMM_KPW_CASES(EPI_RESID_F32, 1)
     case EPI_GEGLU_BF16: UAD_GEMM_KPW_CASES(EPI_GEGLU_BF16, 2)
     case EPI_QKV: UAD_GEMM_KPW_CASES(EPI_QKV, 1)
   }

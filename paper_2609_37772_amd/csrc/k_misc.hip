@@ -1,7 +1,6 @@
 // Per-token kernels of the step: the per-token time embedding and action
-// input projection, the K-split reduction fused with the residual add and the
-// next RMSNorm, and the final norm + action projection fused with the masked
-// per-token Euler update.
+// input projection, and the final norm + action projection fused with the
+// masked per-token Euler update.
 #include "uad_internal.h"
 
 namespace uad {
@@ -43,54 +42,6 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
     const float arg = freqs[j] * tm;
     store_split(te + afrag_index(m, d + j, KB), plane, sinf(arg));
     store_split(te + afrag_index(m, d + half + j, KB), plane, cosf(arg));
-  }
-}
-
-// Row m: h = (bias | h) + (p_0 + p_1 + ... ) over the S K-split partials of
-// the projection, then (if gain) the next GEMM operand n = RMSNorm(h) * gain.
-// NC = columns per thread (d <= 256*NC).  Every load is unconditional (index
-// clamped into the row, masked afterwards) so all of them issue back to back.
-template <int NC, int S>
-__global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs r) {
-  __shared__ float scratch[4];
-  const int m = blockIdx.x;
-  const int d = r.d;
-  float *__restrict__ hr = r.h + (size_t)m * d;
-  const float *__restrict__ basep = r.bias ? r.bias : hr;  // one pointer: no branch between two loads
-  const float *__restrict__ part = r.part + (size_t)m * d;
-  const size_t pstride = (size_t)r.part_rows * d;
-  float base[NC], pv[S][NC];
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int c = min(threadIdx.x + 256 * i, d - 1);
-    base[i] = basep[c];
-#pragma unroll
-    for (int s2 = 0; s2 < S; ++s2) pv[s2][i] = part[s2 * pstride + c];
-  }
-  float hv[NC];
-  float ss = 0.f;
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    float acc = 0.f;
-#pragma unroll
-    for (int s2 = 0; s2 < S; ++s2) acc += pv[s2][i];
-    const bool ok = threadIdx.x + 256 * i < d;
-    hv[i] = ok ? base[i] + acc : 0.f;
-    ss += hv[i] * hv[i];
-  }
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c < d) hr[c] = hv[i];
-  }
-  if (!r.gain) return;
-  ss = block_sum_256(ss, scratch);
-  const float rstd = 1.0f / sqrtf(ss / (float)d + r.eps);
-  const int KB = d / kTileK;
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c < d) store_split(r.n + afrag_index(m, c, KB), r.n_plane, hv[i] * rstd * r.gain[c]);
   }
 }
 
@@ -179,32 +130,6 @@ hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, con
                        hipEvent_t ev0, hipEvent_t ev1) {
   UAD_LAUNCH(temb_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, plane);
   return hipGetLastError();
-}
-
-template <int NC>
-static hipError_t launch_reduce_nc(const ReduceArgs &r, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  switch (r.splits) {
-    case 1: UAD_LAUNCH((reduce_kernel<NC, 1>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
-    case 2: UAD_LAUNCH((reduce_kernel<NC, 2>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
-    case 4: UAD_LAUNCH((reduce_kernel<NC, 4>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
-    case 8: UAD_LAUNCH((reduce_kernel<NC, 8>), dim3(r.M), dim3(256), 0, s, ev0, ev1, r); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_reduce(const ReduceArgs &r, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  switch ((r.d + 255) / 256) {
-    case 1: return launch_reduce_nc<1>(r, s, ev0, ev1);
-    case 2: return launch_reduce_nc<2>(r, s, ev0, ev1);
-    case 3: return launch_reduce_nc<3>(r, s, ev0, ev1);
-    case 4: return launch_reduce_nc<4>(r, s, ev0, ev1);
-    case 5: return launch_reduce_nc<5>(r, s, ev0, ev1);
-    case 6: return launch_reduce_nc<6>(r, s, ev0, ev1);
-    case 7: return launch_reduce_nc<7>(r, s, ev0, ev1);
-    case 8: return launch_reduce_nc<8>(r, s, ev0, ev1);
-  }
-  return hipErrorInvalidValue;
 }
 
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {

@@ -94,11 +94,10 @@ struct Carve {
 };
 
 // Kernel classes reported by the measurement hook.
-enum KClass { K_TEMB, K_GEMM_TIME_IN, K_GEMM_TIME_OUT, K_REDUCE, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP,
+enum KClass { K_TEMB, K_GEMM_TIME_IN, K_GEMM_TIME_OUT, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP,
               K_GEMM_DOWN, K_FINAL, K_NCLASS };
-const char *kClassNames[K_NCLASS] = {"temb", "gemm_time_in", "gemm_time_out", "reduce_norm", "gemm_qkv", "attention",
+const char *kClassNames[K_NCLASS] = {"temb", "gemm_time_in", "gemm_time_out", "gemm_qkv", "attention",
                                      "gemm_o", "gemm_gateup", "gemm_down", "final_euler"};
-constexpr int kMaxSplits = 8;
 
 hipEvent_t pool_event(uad_ctx *c) {
   if (!c->ev_pool.empty()) {
@@ -266,11 +265,11 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   const size_t M = c->m_alloc;
   Carve a;
   // GEMM inputs (te, z, n, o, g) hold two bf16 planes (hi, lo) of M rows each;
-  // part holds the K-split partial sums of the projections that feed the residual stream
+  // ssq holds the per-16-column sums of squares of h (RMSNorm folded into the GEMMs)
   size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(2 * M * 2 * d), o_z = a.take<uint16_t>(2 * M * d),
          o_n = a.take<uint16_t>(2 * M * d), o_o = a.take<uint16_t>(2 * M * c->q_dim), o_g = a.take<uint16_t>(2 * M * F),
          o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
-         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_part = a.take<float>((size_t)kMaxSplits * M * d);
+         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -287,7 +286,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->q = (__bf16 *)(ab + o_q);
   c->attn_opart = (float *)(ab + o_op);
   c->attn_ml = (float *)(ab + o_ml);
-  c->part = (float *)(ab + o_part);
+  c->ssq = (float *)(ab + o_ssq);
   e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
   if (e != hipSuccess) {
     uad_destroy(c);
@@ -510,9 +509,10 @@ static uad_status check_step_args(uad_ctx *c, const void *x, const void *t, cons
 
 // Enqueue one joint step on stream s: F_theta over all B*H tokens, then the
 // masked Euler update.  Kernel sequence: temb -> time-MLP in -> time-MLP out
-// (K-split partials) -> reduce (+RMSNorm) -> per layer [QKV -> attention ->
-// O (partials) -> reduce (+RMSNorm) -> gate/up GeGLU -> down (partials) ->
-// reduce (+RMSNorm of the next layer)] -> final norm/projection/Euler.
+// (+ residual init, RMSNorm sums, next operand) -> per layer [QKV (x rstd) ->
+// attention (+ split-KV combine) -> O (+ residual, sums, next operand) ->
+// gate/up GeGLU (x rstd) -> down (+ residual, sums, next layer's operand)] ->
+// final norm/projection/Euler.
 static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float *t, const float *dt,
                                const uint8_t *mask, const uint8_t *next_mask, int is_last, int step, float *v_out,
                                float *released, int32_t *release_step, int B, int H) {
@@ -535,21 +535,21 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
   if (!c->dbg) {
     UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
                                       MA * 2 * d, s, ea_, eb_));
+    // RMSNorm folding: residual GEMMs write ssq and the next operand; consumers scale by rstd
+    auto norm_fields = [&](GemmArgs &x) {
+      x.ssq = c->ssq; x.ssq_tiles = d / 16; x.m_alloc = (int)MA; x.eps = c->cfg.rms_eps;
+    };
     GemmArgs g{};
     g.M = M;
     g.A = c->a_te; g.a_plane = MA * 2 * d; g.W = c->t1_w; g.N = d; g.K = 2 * d;
     g.out = c->a_z; g.ldo = d; g.out_plane = MA * d; g.bias = c->t1_b;
-    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU_BF16, g, plan_gemm(EPI_BIAS_SILU_BF16, M, d, 2 * d,
-                                                                              kMaxSplits), s, ea_, eb_));
+    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU_BF16, g, plan_gemm(EPI_BIAS_SILU_BF16, M, d, 2 * d), s,
+                                              ea_, eb_));
     GemmArgs g2{};
     g2.M = M; g2.A = c->a_z; g2.a_plane = MA * d; g2.W = c->t2_w; g2.N = d; g2.K = d;
-    g2.out = c->part; g2.ldo = d; g2.part_rows = (int)MA;
-    const GemmPlan p2 = plan_gemm(EPI_PARTIAL_F32, M, d, d, kMaxSplits);
-    UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_PARTIAL_F32, g2, p2, s, ea_, eb_));
-    ReduceArgs r{};
-    r.h = c->h; r.part = c->part; r.splits = p2.splits; r.part_rows = (int)MA; r.M = M; r.d = d;
-    r.bias = c->t2_b; r.gain = c->layers[0].attn_norm; r.eps = c->cfg.rms_eps; r.n = c->a_n; r.n_plane = MA * d;
-    UAD_CHECK_CLS(K_REDUCE, launch_reduce(r, s, ea_, eb_));
+    g2.out = c->h; g2.ldo = d; g2.bias = c->t2_b; norm_fields(g2);
+    g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n; g2.next_plane = MA * d;
+    UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_RESID_F32, g2, plan_gemm(EPI_RESID_F32, M, d, d), s, ea_, eb_));
 
     AttnArgs at{};
     at.q = c->q; at.ldq = c->q_dim; at.s_alloc = c->s_alloc; at.n_keys = c->prefix_len + H;
@@ -559,10 +559,10 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
     at.o = c->a_o; at.ldo = c->q_dim; at.o_plane = MA * c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
 
-    const GemmPlan pq = plan_gemm(EPI_QKV, M, c->n_qkv, d, kMaxSplits);
-    const GemmPlan po = plan_gemm(EPI_PARTIAL_F32, M, d, c->q_dim, kMaxSplits);
-    const GemmPlan pg = plan_gemm(EPI_GEGLU_BF16, M, 2 * F, d, kMaxSplits);
-    const GemmPlan pd = plan_gemm(EPI_PARTIAL_F32, M, d, F, kMaxSplits);
+    const GemmPlan pq = plan_gemm(EPI_QKV, M, c->n_qkv, d);
+    const GemmPlan po = plan_gemm(EPI_RESID_F32, M, d, c->q_dim);
+    const GemmPlan pg = plan_gemm(EPI_GEGLU_BF16, M, 2 * F, d);
+    const GemmPlan pd = plan_gemm(EPI_RESID_F32, M, d, F);
     for (int l = 0; l < c->L; ++l) {
       const uad_layer_ptrs &lp = c->layers[l];
       __bf16 *kc = c->kcache + l * c->kv_layer_elems;
@@ -571,25 +571,24 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       q.M = M; q.A = c->a_n; q.a_plane = MA * d; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
+      norm_fields(q); q.use_rstd = 1;
       UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, pq, s, ea_, eb_));
       at.kc = kc; at.vtc = vtc;
       UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s, ea_, eb_));
       GemmArgs o{};
       o.M = M; o.A = c->a_o; o.a_plane = MA * c->q_dim; o.W = lp.wo; o.N = d; o.K = c->q_dim;
-      o.out = c->part; o.ldo = d; o.part_rows = (int)MA;
-      UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_PARTIAL_F32, o, po, s, ea_, eb_));
-      r.bias = nullptr; r.splits = po.splits; r.gain = lp.mlp_norm;
-      UAD_CHECK_CLS(K_REDUCE, launch_reduce(r, s, ea_, eb_));
+      o.out = c->h; o.ldo = d; norm_fields(o);
+      o.gain_next = lp.mlp_norm; o.next = c->a_n; o.next_plane = MA * d;
+      UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, po, s, ea_, eb_));
       GemmArgs gu{};
       gu.M = M; gu.A = c->a_n; gu.a_plane = MA * d; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
-      gu.out = c->a_g; gu.ldo = F; gu.out_plane = MA * F;
+      gu.out = c->a_g; gu.ldo = F; gu.out_plane = MA * F; norm_fields(gu); gu.use_rstd = 1;
       UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU_BF16, gu, pg, s, ea_, eb_));
       GemmArgs dn{};
       dn.M = M; dn.A = c->a_g; dn.a_plane = MA * F; dn.W = lp.wdown; dn.N = d; dn.K = F;
-      dn.out = c->part; dn.ldo = d; dn.part_rows = (int)MA;
-      UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_PARTIAL_F32, dn, pd, s, ea_, eb_));
-      r.splits = pd.splits; r.gain = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr;
-      UAD_CHECK_CLS(K_REDUCE, launch_reduce(r, s, ea_, eb_));
+      dn.out = c->h; dn.ldo = d; norm_fields(dn);
+      dn.gain_next = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr; dn.next = c->a_n; dn.next_plane = MA * d;
+      UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_RESID_F32, dn, pd, s, ea_, eb_));
     }
   }
   FinalArgs f{};

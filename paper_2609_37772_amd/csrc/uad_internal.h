@@ -64,17 +64,17 @@ __host__ __device__ __forceinline__ size_t afrag_index(int r, int c, int KB) {
 // ---------------------------------------------------------------------------
 enum Epilogue : int {
   EPI_BIAS_SILU_BF16 = 0,  // out = split bf16 planes of silu(acc + bias), fragment order
-  EPI_PARTIAL_F32 = 1,     // out[split][row][col] = fp32 partial sum over this K split
-  EPI_GEGLU_BF16 = 3,      // out = split planes of gelu_tanh(acc_gate) * acc_up (tile-interleaved gate/up)
-  EPI_QKV = 4,             // q -> bf16 q buffer; k, v -> per-layer K / V^T store
+  EPI_RESID_F32 = 1,       // h = (bias | h) + acc; per-tile sum of squares; next operand split(h * gain_next)
+  EPI_GEGLU_BF16 = 3,      // out = split planes of gelu_tanh(rstd*acc_gate) * rstd*acc_up (interleaved gate/up)
+  EPI_QKV = 4,             // rstd*acc: q -> bf16 q buffer; k, v -> per-layer K / V^T store
 };
 
 struct GemmPlan {
-  int T;       // 16-column weight tiles per workgroup
-  int splits;  // K splits (grid.y)
-  int kpw;     // 32-deep k-blocks per wave and pass
-  int waves;   // waves per workgroup
-  int passes;  // runs of kpw blocks per wave
+  int T;        // 16-column weight tiles per workgroup
+  int mgroups;  // row groups (grid.z); group z owns 16-row tiles [z*MT/mgroups, (z+1)*MT/mgroups)
+  int kpw;      // 32-deep k-blocks per wave and pass
+  int waves;    // waves per workgroup
+  int passes;   // runs of kpw blocks per wave
   bool ok;
 };
 
@@ -83,7 +83,16 @@ struct GemmArgs {
   int lda;
   size_t a_plane;   // element offset of the lo plane
   size_t out_plane; // element offset of the lo plane of a split bf16 output
-  int part_rows;    // row stride between K-split partials (EPI_PARTIAL_F32)
+  // RMSNorm folded into the GEMMs: a residual GEMM writes ssq[tile][row] (sum of
+  // squares of h over its 16 columns) and the next operand split(h * gain_next);
+  // a consuming GEMM scales its accumulator by rstd[row] from those sums.
+  float *ssq;             // [d/16][m_alloc]
+  int ssq_tiles, m_alloc;
+  float eps;
+  const float *gain_next; // EPI_RESID_F32: gain of the following RMSNorm (nullptr: none)
+  __bf16 *next;           // EPI_RESID_F32: next operand, split planes, fragment order (K = N)
+  size_t next_plane;
+  int use_rstd;           // EPI_QKV / EPI_GEGLU_BF16: scale by rstd from ssq
   const __bf16 *W;  // packed weights, N/16 tiles x K/32 blocks
   int M, N, K;      // N counts packed output columns (2F for gate/up)
   void *out;        // epilogue destination
@@ -112,19 +121,6 @@ struct AttnArgs {
   float *mlpart;     // [splits][B*Hkv][rows_pad][2]
 };
 
-// h = (bias or h) + sum of K-split partials (fixed order); optionally the next
-// GEMM's operand n = split planes of RMSNorm(h) * gain, in fragment order.
-struct ReduceArgs {
-  float *h;            // [M][d]
-  const float *part;   // [splits][part_rows][d]
-  int splits, part_rows, M, d;
-  const float *bias;   // non-null: h = bias + sum (initialisation)
-  const float *gain;   // non-null: write n
-  float eps;
-  __bf16 *n;
-  size_t n_plane;
-};
-
 struct FinalArgs {
   const float *h;       // [M][d]
   const float *gain;    // final_norm [d]
@@ -148,12 +144,11 @@ struct FinalArgs {
 // ---------------------------------------------------------------------------
 // Launchers (defined in the .hip translation units)
 // ---------------------------------------------------------------------------
-GemmPlan plan_gemm(int epi, int M, int N, int K, int max_splits);
+GemmPlan plan_gemm(int epi, int M, int N, int K);
 // ev0 / ev1: optional events recorded at the start / end of the launched
 // kernel(s) (nullptr for none).
 hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_t s, hipEvent_t ev0 = nullptr,
                        hipEvent_t ev1 = nullptr);
-hipError_t launch_reduce(const ReduceArgs &r, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0 = nullptr,
                             hipEvent_t ev1 = nullptr);
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
@@ -226,7 +221,7 @@ struct uad_ctx {
   __bf16 *a_te = nullptr, *a_z = nullptr, *a_n = nullptr, *a_o = nullptr, *a_g = nullptr, *q = nullptr;
   float *attn_opart = nullptr, *attn_ml = nullptr;
   size_t attn_part_elems = 0;
-  float *part = nullptr;  // K-split partials [splits][m_alloc][d]
+  float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]
   void *abuf = nullptr;
 
   // captured step / schedule graphs (small LRU cache)
