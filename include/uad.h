@@ -107,12 +107,16 @@ uad_status uad_set_stream(uad_ctx *ctx, void *hip_stream);
 
 /* Load the action-expert parameters theta of F_theta (Sec. 3 Eq. 1).
  * `tensors` must name every weight listed at the top exactly once, with the
- * listed shape; dtype F32 or BF16 (F32 values are rounded to bf16,
- * nearest-even, for the large projections; norm gains, biases and the
- * action in/out projections are kept in fp32).  The data are COPIED into
+ * listed shape; dtype F32 or BF16.  The large projections (time MLP, QKV, O,
+ * gate/up, down) are rounded once to bf16 (nearest-even; a no-op for BF16
+ * input) and held as fp16, which represents every bf16 value of magnitude in
+ * [2^-14, 65504] exactly; smaller magnitudes round to the nearest fp16
+ * subnormal (absolute error <= 2^-25).  Norm gains, biases and the action
+ * in/out projections are kept in fp32.  The data are COPIED into
  * library-owned device memory in the kernels' packed layout; the caller may
  * free its buffers on return.  Synchronous.  Errors: UAD_E_MISSING (absent or
- * duplicated name, named in the message), UAD_E_SHAPE, UAD_E_INVALID, UAD_E_HIP. */
+ * duplicated name, named in the message), UAD_E_SHAPE, UAD_E_INVALID (bad
+ * dtype, or a projection weight that is NaN or beyond +-65504), UAD_E_HIP. */
 uad_status uad_load_weights(uad_ctx *ctx, const uad_tensor *tensors, int32_t n_tensors);
 
 /* Set the cached context of the action expert: the per-layer key/value

@@ -193,8 +193,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       const float inv = 1.0f / lr[r];
 #pragma unroll
       for (int nt = 0; nt < NTO; ++nt)
-        store_split(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), a.o_plane,
-                    o[nt][r] * inv);
+        store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv);
     }
   } else {
     const size_t pbase = ((size_t)split * gridDim.z + eh) * a.rows_pad;
@@ -249,7 +248,7 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a) {
   }
   const int hg = row / a.chunk, tok = row - hg * a.chunk;
   const int head = g * a.group + hg;
-  store_split(a.o + afrag_index(b * a.chunk + tok, head * HD + c, a.ldo / kTileK), a.o_plane, num / den);
+  store_op(a.o + afrag_index(b * a.chunk + tok, head * HD + c, a.ldo / kTileK), num / den);
 }
 
 template <int HD>

@@ -1,5 +1,5 @@
 // Projection GEMMs of the action expert: C[M][N] = A[M][K] * W[N][K]^T on the
-// gfx950 MFMA units (v_mfma_f32_16x16x32_bf16), fp32 accumulation, with the
+// gfx950 MFMA units (v_mfma_f32_16x16x32_f16), fp32 accumulation, with the
 // epilogue of the layer fused in.
 //
 // Shape of the work: M is the token count (B*H: 16..3200), N and K are the
@@ -14,13 +14,11 @@
 //     a run (weights and activations) before its first MFMA;
 //   * weights and activations are both stored in MFMA fragment order, so each
 //     operand load is one aligned 16-byte load per lane, 1 KiB per wave;
-//   * activations are hi/lo bf16 planes: every weight fragment feeds two
-//     MFMAs (the MFMA units idle at batch 1, HBM does not);
 //   * per-wave partial tiles are reduced through LDS in fixed wave order
 //     (deterministic, no atomics).
 // RMSNorm is folded into the GEMMs: the residual GEMMs (time-MLP out, O, down)
 // update h for their columns, write the per-16-column sum of squares of every
-// row and the next operand split(h * gain_next); the GEMMs that consume a
+// row and the next operand fp16(h * gain_next); the GEMMs that consume a
 // normalised input (QKV, gate/up) scale their accumulators by
 // rstd[row] = (sum of those sums / d + eps)^-1/2, since
 // RMSNorm(h) W^T = rstd * ((h * gain) W^T).
@@ -58,7 +56,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   // (the first 16 tiles of each wave are unconditional loads with clamped
   // indices so they issue back to back; d/16 tiles need more only when fewer
   // than d/256 waves run)
-  if ((EPI == EPI_QKV || EPI == EPI_GEGLU_BF16) && g.use_rstd) {
+  if ((EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd) {
     const int row = min(m0 + lane, g.M - 1);
     float vals[16];
 #pragma unroll
@@ -82,27 +80,18 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 
   for (int pass = 0; pass < passes; ++pass) {
     const int kb0 = (pass * waves + wave) * KPW;
-    bf16x8 w[KPW][T], ah[KPW][kMaxTilesPerGroup], al[KPW][kMaxTilesPerGroup];
-    const __bf16 *wp = g.W + ((size_t)tile0 * KB + kb0) * kBlockElems + lane * 8;
+    f16x8 w[KPW][T], a[KPW][kMaxTilesPerGroup];
+    const op_t *wp = g.W + ((size_t)tile0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
     for (int j = 0; j < KPW; ++j)
 #pragma unroll
-      for (int t = 0; t < T; ++t) w[j][t] = *(const bf16x8 *)(wp + ((size_t)t * KB + j) * kBlockElems);
-    const __bf16 *ap = g.A + ((size_t)mt0 * KB + kb0) * kBlockElems + lane * 8;
+      for (int t = 0; t < T; ++t) w[j][t] = *(const f16x8 *)(wp + ((size_t)t * KB + j) * kBlockElems);
+    const op_t *ap = g.A + ((size_t)mt0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
     for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
       const bool ok = mt < nmt && (m0 + mt * 16 + (lane & 15)) < g.M;
 #pragma unroll
-      for (int j = 0; j < KPW; ++j) {
-        if (ok) {
-          const __bf16 *p = ap + ((size_t)mt * KB + j) * kBlockElems;
-          ah[j][mt] = *(const bf16x8 *)p;
-          al[j][mt] = *(const bf16x8 *)(p + g.a_plane);
-        } else {
-          ah[j][mt] = bf16x8{};
-          al[j][mt] = bf16x8{};
-        }
-      }
+      for (int j = 0; j < KPW; ++j) a[j][mt] = ok ? *(const f16x8 *)(ap + ((size_t)mt * KB + j) * kBlockElems) : f16x8{};
     }
 #pragma unroll
     for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
@@ -110,10 +99,8 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int j = 0; j < KPW; ++j)
 #pragma unroll
-        for (int t = 0; t < T; ++t) {
-          acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j][mt], w[j][t], acc[mt][t], 0, 0, 0);
-          acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j][mt], w[j][t], acc[mt][t], 0, 0, 0);
-        }
+        for (int t = 0; t < T; ++t)
+          acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[j][mt], w[j][t], acc[mt][t], 0, 0, 0);
     }
   }
 
@@ -126,7 +113,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[((wave * SLOTS) + (mt * T + t) * 4 + r) * 64 + lane] = acc[mt][t][r];
   __syncthreads();
-  if ((EPI == EPI_QKV || EPI == EPI_GEGLU_BF16) && g.use_rstd && threadIdx.x < 64) {
+  if ((EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd && threadIdx.x < 64) {
     float ss = 0.f;
     for (int w2 = 0; w2 < waves; ++w2) ss += rpart[w2][threadIdx.x];
     rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
@@ -137,14 +124,14 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   // GeGLU slot = (mt*(T/2) + pair)*4 + r); the D fragment of a 16x16 MFMA holds
   // row 4*(lane>>4)+r, column lane&15.  The per-wave trip count is uniform and
   // the 16 lanes holding one row are always active together.
-  const int n_out = (EPI == EPI_GEGLU_BF16) ? nmt * 256 * (T / 2) : nmt * 256 * T;
+  const int n_out = (EPI == EPI_GEGLU) ? nmt * 256 * (T / 2) : nmt * 256 * T;
   for (int e0 = 0; e0 < n_out; e0 += blockDim.x) {
     const int e = e0 + threadIdx.x;
     if (e >= n_out) continue;  // whole waves only (n_out and blockDim are multiples of 64)
     const int ln = e & 63;
     const int slot = e >> 6;
     int mt, t, r;
-    if (EPI == EPI_GEGLU_BF16) {
+    if (EPI == EPI_GEGLU) {
       r = slot & 3;
       const int q = slot >> 2;
       t = 2 * (q % (T / 2));
@@ -173,24 +160,22 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
       if (row_ok) {
         if ((ln & 15) == 0) g.ssq[(size_t)(tile0 + t) * g.m_alloc + row] = sq;
-        if (g.gain_next)
-          store_split(g.next + afrag_index(row, col, g.N / kTileK), g.next_plane, hv * g.gain_next[col]);
+        if (g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * g.gain_next[col]);
       }
       continue;
     }
     if (!row_ok) continue;
-    const float rs = ((EPI == EPI_QKV || EPI == EPI_GEGLU_BF16) && g.use_rstd) ? rstd_s[rl] : 1.0f;
-    if (EPI == EPI_GEGLU_BF16) {
+    const float rs = ((EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd) ? rstd_s[rl] : 1.0f;
+    if (EPI == EPI_GEGLU) {
       const int s1 = (mt * T + t + 1) * 4 + r;
       float u = 0.f;
       for (int w2 = 0; w2 < waves; ++w2) u += red[(w2 * SLOTS + s1) * 64 + ln];
       const int col = ((tile0 + t) >> 1) * 16 + (ln & 15);
-      store_split((__bf16 *)g.out + afrag_index(row, col, g.ldo / kTileK), g.out_plane,
-                  gelu_tanh(v * rs) * (u * rs));
+      store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), gelu_tanh(v * rs) * (u * rs));
     } else {
       const int col = (tile0 + t) * 16 + (ln & 15);
-      if (EPI == EPI_BIAS_SILU_BF16) {
-        store_split((__bf16 *)g.out + afrag_index(row, col, g.ldo / kTileK), g.out_plane, silu(v + g.bias[col]));
+      if (EPI == EPI_BIAS_SILU) {
+        store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), silu(v + g.bias[col]));
       } else if (EPI == EPI_QKV) {
         v *= rs;
         if (col < g.q_dim) {
@@ -230,7 +215,7 @@ static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, 
 GemmPlan plan_gemm(int epi, int M, int N, int K) {
   GemmPlan p{};
   const int KB = K / kTileK;
-  p.T = (epi == EPI_GEGLU_BF16) ? 2 : 1;
+  p.T = (epi == EPI_GEGLU) ? 2 : 1;
   const int ngroups = N / kTileN / p.T;
   const int MT = (M + 15) / 16;
   if (MT > kMaxTilesPerGroup) {
@@ -265,9 +250,9 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
                        hipEvent_t ev1) {
   if (!p.ok) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_BIAS_SILU_BF16: UAD_GEMM_KPW_CASES(EPI_BIAS_SILU_BF16, 1)
+    case EPI_BIAS_SILU: UAD_GEMM_KPW_CASES(EPI_BIAS_SILU, 1)
     case EPI_RESID_F32: UAD_GEMM_KPW_CASES(EPI_RESID_F32, 1)
-    case EPI_GEGLU_BF16: UAD_GEMM_KPW_CASES(EPI_GEGLU_BF16, 2)
+    case EPI_GEGLU: UAD_GEMM_KPW_CASES(EPI_GEGLU, 2)
     case EPI_QKV: UAD_GEMM_KPW_CASES(EPI_QKV, 1)
   }
   return hipErrorInvalidValue;

@@ -17,14 +17,13 @@ __device__ __forceinline__ float block_sum_256(float v, float *scratch) {
   return (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
 }
 
-// te[m] = [ x_m W_in^T + b_in ; sin(w t_m) ; cos(w t_m) ] as split bf16 planes in
-// fragment order (K = 2d): the per-token flow-time conditioning placed before
-// the action MLP.
+// te[m] = [ x_m W_in^T + b_in ; sin(w t_m) ; cos(w t_m) ] as the fp16 operand
+// of the time MLP in fragment order (K = 2d): the per-token flow-time
+// conditioning placed before the action MLP.
 __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, const float *__restrict__ t,
                                                     int Da, int d, const float *__restrict__ w_in,
                                                     const float *__restrict__ b_in,
-                                                    const float *__restrict__ freqs, __bf16 *__restrict__ te,
-                                                    size_t plane) {
+                                                    const float *__restrict__ freqs, op_t *__restrict__ te) {
   __shared__ float xs[64];
   const int m = blockIdx.x;
   const int KB = 2 * d / kTileK;
@@ -34,14 +33,14 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
     float acc = b_in[n];
     const float *w = w_in + (size_t)n * Da;
     for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
-    store_split(te + afrag_index(m, n, KB), plane, acc);
+    store_op(te + afrag_index(m, n, KB), acc);
   }
   const float tm = t[m];
   const int half = d >> 1;
   for (int j = threadIdx.x; j < half; j += blockDim.x) {
     const float arg = freqs[j] * tm;
-    store_split(te + afrag_index(m, d + j, KB), plane, sinf(arg));
-    store_split(te + afrag_index(m, d + half + j, KB), plane, cosf(arg));
+    store_op(te + afrag_index(m, d + j, KB), sinf(arg));
+    store_op(te + afrag_index(m, d + half + j, KB), cosf(arg));
   }
 }
 
@@ -126,9 +125,9 @@ __global__ void stamp_kernel(uint64_t *dst) {
 }
 
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
-                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s,
+                       const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
-  UAD_LAUNCH(temb_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, plane);
+  UAD_LAUNCH(temb_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te);
   return hipGetLastError();
 }
 

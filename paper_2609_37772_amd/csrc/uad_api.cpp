@@ -69,18 +69,31 @@ bool fetch_f32(const void *data, int dtype, int on_device, size_t n, std::vector
   return true;
 }
 
+// A projection weight as the kernels hold it: the value rounded once to bf16
+// (the model's precision), then stored as fp16, which is exact for bf16
+// magnitudes in [2^-14, 65504]; smaller ones round to the nearest fp16
+// subnormal.  Returns false for magnitudes beyond the fp16 range (or NaN).
+bool weight_to_f16(float w, _Float16 *out) {
+  const float b = bf16_to_f32(f32_to_bf16_rne(w));
+  if (!(std::fabs(b) <= 65504.0f)) return false;
+  *out = (_Float16)b;
+  return true;
+}
+
 // Pack row-major W[N][K] into the MFMA fragment order (see uad_internal.h),
 // writing 16-row tile nt to destination tile (tile_base + nt * tile_step).
-void pack_tiles(const float *W, int N, int K, uint16_t *dst, int tile_base, int tile_step) {
+bool pack_tiles(const float *W, int N, int K, _Float16 *dst, int tile_base, int tile_step) {
   const int KB = K / kTileK;
+  bool ok = true;
   for (int nt = 0; nt < N / kTileN; ++nt) {
-    uint16_t *tb = dst + (size_t)(tile_base + nt * tile_step) * KB * kBlockElems;
+    _Float16 *tb = dst + (size_t)(tile_base + nt * tile_step) * KB * kBlockElems;
     for (int kb = 0; kb < KB; ++kb)
       for (int l = 0; l < 64; ++l)
         for (int e = 0; e < 8; ++e)
-          tb[((size_t)kb * 64 + l) * 8 + e] =
-              f32_to_bf16_rne(W[(size_t)(nt * kTileN + (l & 15)) * K + kb * kTileK + (l >> 4) * 8 + e]);
+          ok &= weight_to_f16(W[(size_t)(nt * kTileN + (l & 15)) * K + kb * kTileK + (l >> 4) * 8 + e],
+                              &tb[((size_t)kb * 64 + l) * 8 + e]);
   }
+  return ok;
 }
 
 struct Carve {
@@ -217,13 +230,13 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->action_out_w = (float *)(wb + o_aout);
   c->action_out_b = (float *)(wb + o_aoutb);
   c->freqs = (float *)(wb + o_freq);
-  c->t1_w = (__bf16 *)(wb + o_t1);
-  c->t2_w = (__bf16 *)(wb + o_t2);
+  c->t1_w = (op_t *)(wb + o_t1);
+  c->t2_w = (op_t *)(wb + o_t2);
   for (int l = 0; l < c->L; ++l) {
-    c->layers[l].wqkv = (const __bf16 *)(wb + o_l[6 * l + 0]);
-    c->layers[l].wo = (const __bf16 *)(wb + o_l[6 * l + 1]);
-    c->layers[l].wgu = (const __bf16 *)(wb + o_l[6 * l + 2]);
-    c->layers[l].wdown = (const __bf16 *)(wb + o_l[6 * l + 3]);
+    c->layers[l].wqkv = (const op_t *)(wb + o_l[6 * l + 0]);
+    c->layers[l].wo = (const op_t *)(wb + o_l[6 * l + 1]);
+    c->layers[l].wgu = (const op_t *)(wb + o_l[6 * l + 2]);
+    c->layers[l].wdown = (const op_t *)(wb + o_l[6 * l + 3]);
     c->layers[l].attn_norm = (const float *)(wb + o_l[6 * l + 4]);
     c->layers[l].mlp_norm = (const float *)(wb + o_l[6 * l + 5]);
   }
@@ -264,10 +277,10 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->attn_part_elems = part;
   const size_t M = c->m_alloc;
   Carve a;
-  // GEMM inputs (te, z, n, o, g) hold two bf16 planes (hi, lo) of M rows each;
+  // GEMM inputs (te, z, n, o, g) are fp16 in fragment order, M rows each;
   // ssq holds the per-16-column sums of squares of h (RMSNorm folded into the GEMMs)
-  size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(2 * M * 2 * d), o_z = a.take<uint16_t>(2 * M * d),
-         o_n = a.take<uint16_t>(2 * M * d), o_o = a.take<uint16_t>(2 * M * c->q_dim), o_g = a.take<uint16_t>(2 * M * F),
+  size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(M * 2 * d), o_z = a.take<uint16_t>(M * d),
+         o_n = a.take<uint16_t>(M * d), o_o = a.take<uint16_t>(M * c->q_dim), o_g = a.take<uint16_t>(M * F),
          o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
          o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M);
   e = hipMalloc(&c->abuf, a.off);
@@ -278,11 +291,11 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   }
   char *ab = (char *)c->abuf;
   c->h = (float *)(ab + o_h);
-  c->a_te = (__bf16 *)(ab + o_te);
-  c->a_z = (__bf16 *)(ab + o_z);
-  c->a_n = (__bf16 *)(ab + o_n);
-  c->a_o = (__bf16 *)(ab + o_o);
-  c->a_g = (__bf16 *)(ab + o_g);
+  c->a_te = (op_t *)(ab + o_te);
+  c->a_z = (op_t *)(ab + o_z);
+  c->a_n = (op_t *)(ab + o_n);
+  c->a_o = (op_t *)(ab + o_o);
+  c->a_g = (op_t *)(ab + o_g);
   c->q = (__bf16 *)(ab + o_q);
   c->attn_opart = (float *)(ab + o_op);
   c->attn_ml = (float *)(ab + o_ml);
@@ -392,7 +405,8 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
     return e == hipSuccess;
   };
   std::vector<float> v1, v2, v3;
-  std::vector<uint16_t> pk;
+  std::vector<_Float16> pk;
+  bool range_ok = true;  // every projection weight within the fp16 range
   auto put_f32 = [&](const std::string &name, float *dst) {
     return host(name, &v1) && up(dst, v1.data(), v1.size() * 4);
   };
@@ -402,12 +416,12 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
             put_f32("action_out.b", c->action_out_b);
   if (ok && (ok = host("time_mlp_in.w", &v1))) {
     pk.assign((size_t)d * 2 * d, 0);
-    pack_tiles(v1.data(), d, 2 * d, pk.data(), 0, 1);
+    range_ok &= pack_tiles(v1.data(), d, 2 * d, pk.data(), 0, 1);
     ok = up(c->t1_w, pk.data(), pk.size() * 2);
   }
   if (ok && (ok = host("time_mlp_out.w", &v1))) {
     pk.assign((size_t)d * d, 0);
-    pack_tiles(v1.data(), d, d, pk.data(), 0, 1);
+    range_ok &= pack_tiles(v1.data(), d, d, pk.data(), 0, 1);
     ok = up(c->t2_w, pk.data(), pk.size() * 2);
   }
   for (int l = 0; ok && l < c->L; ++l) {
@@ -419,34 +433,38 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
     pk.assign((size_t)c->n_qkv * d, 0);
     ok = host(p + "wq", &v1) && host(p + "wk", &v2) && host(p + "wv", &v3);
     if (!ok) break;
-    pack_tiles(v1.data(), c->q_dim, d, pk.data(), 0, 1);
-    pack_tiles(v2.data(), c->kv_dim, d, pk.data(), c->q_dim / kTileN, 1);
-    pack_tiles(v3.data(), c->kv_dim, d, pk.data(), (c->q_dim + c->kv_dim) / kTileN, 1);
+    range_ok &= pack_tiles(v1.data(), c->q_dim, d, pk.data(), 0, 1);
+    range_ok &= pack_tiles(v2.data(), c->kv_dim, d, pk.data(), c->q_dim / kTileN, 1);
+    range_ok &= pack_tiles(v3.data(), c->kv_dim, d, pk.data(), (c->q_dim + c->kv_dim) / kTileN, 1);
     ok = up((void *)lp.wqkv, pk.data(), pk.size() * 2);
     if (!ok) break;
     ok = host(p + "wo", &v1);
     if (!ok) break;
     pk.assign((size_t)d * c->q_dim, 0);
-    pack_tiles(v1.data(), d, c->q_dim, pk.data(), 0, 1);
+    range_ok &= pack_tiles(v1.data(), d, c->q_dim, pk.data(), 0, 1);
     ok = up((void *)lp.wo, pk.data(), pk.size() * 2);
     if (!ok) break;
     // gate/up interleaved per 16-column tile: tile 2j = gate j, tile 2j+1 = up j
     ok = host(p + "w_gate", &v1) && host(p + "w_up", &v2);
     if (!ok) break;
     pk.assign((size_t)2 * F * d, 0);
-    pack_tiles(v1.data(), F, d, pk.data(), 0, 2);
-    pack_tiles(v2.data(), F, d, pk.data(), 1, 2);
+    range_ok &= pack_tiles(v1.data(), F, d, pk.data(), 0, 2);
+    range_ok &= pack_tiles(v2.data(), F, d, pk.data(), 1, 2);
     ok = up((void *)lp.wgu, pk.data(), pk.size() * 2);
     if (!ok) break;
     ok = host(p + "w_down", &v1);
     if (!ok) break;
     pk.assign((size_t)d * F, 0);
-    pack_tiles(v1.data(), d, F, pk.data(), 0, 1);
+    range_ok &= pack_tiles(v1.data(), d, F, pk.data(), 0, 1);
     ok = up((void *)lp.wdown, pk.data(), pk.size() * 2);
   }
   if (!ok) {
     c->weights_loaded = false;
     return fail(c, UAD_E_HIP, "uad_load_weights: " + err);
+  }
+  if (!range_ok) {
+    c->weights_loaded = false;
+    return fail(c, UAD_E_INVALID, "uad_load_weights: a projection weight is NaN or beyond the fp16 range (|w| > 65504)");
   }
   c->weights_loaded = true;
   return UAD_OK;
@@ -533,22 +551,21 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     if (c->prof_on) c->prof_pending.push_back({cls, ea_, eb_}); \
   } while (0)
   if (!c->dbg) {
-    UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
-                                      MA * 2 * d, s, ea_, eb_));
+    UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, s,
+                                      ea_, eb_));
     // RMSNorm folding: residual GEMMs write ssq and the next operand; consumers scale by rstd
     auto norm_fields = [&](GemmArgs &x) {
       x.ssq = c->ssq; x.ssq_tiles = d / 16; x.m_alloc = (int)MA; x.eps = c->cfg.rms_eps;
     };
     GemmArgs g{};
     g.M = M;
-    g.A = c->a_te; g.a_plane = MA * 2 * d; g.W = c->t1_w; g.N = d; g.K = 2 * d;
-    g.out = c->a_z; g.ldo = d; g.out_plane = MA * d; g.bias = c->t1_b;
-    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU_BF16, g, plan_gemm(EPI_BIAS_SILU_BF16, M, d, 2 * d), s,
-                                              ea_, eb_));
+    g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = 2 * d;
+    g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
+    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, 2 * d), s, ea_, eb_));
     GemmArgs g2{};
-    g2.M = M; g2.A = c->a_z; g2.a_plane = MA * d; g2.W = c->t2_w; g2.N = d; g2.K = d;
+    g2.M = M; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d;
     g2.out = c->h; g2.ldo = d; g2.bias = c->t2_b; norm_fields(g2);
-    g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n; g2.next_plane = MA * d;
+    g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n;
     UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_RESID_F32, g2, plan_gemm(EPI_RESID_F32, M, d, d), s, ea_, eb_));
 
     AttnArgs at{};
@@ -557,18 +574,18 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     at.rows = at.group * H; at.rows_pad = (at.rows + 63) / 64 * 64;
     at.splits = attn_splits(c, B, H, c->prefix_len, &at.blocks_per_split);
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
-    at.o = c->a_o; at.ldo = c->q_dim; at.o_plane = MA * c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
+    at.o = c->a_o; at.ldo = c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
 
     const GemmPlan pq = plan_gemm(EPI_QKV, M, c->n_qkv, d);
     const GemmPlan po = plan_gemm(EPI_RESID_F32, M, d, c->q_dim);
-    const GemmPlan pg = plan_gemm(EPI_GEGLU_BF16, M, 2 * F, d);
+    const GemmPlan pg = plan_gemm(EPI_GEGLU, M, 2 * F, d);
     const GemmPlan pd = plan_gemm(EPI_RESID_F32, M, d, F);
     for (int l = 0; l < c->L; ++l) {
       const uad_layer_ptrs &lp = c->layers[l];
       __bf16 *kc = c->kcache + l * c->kv_layer_elems;
       __bf16 *vtc = c->vtcache + l * c->kv_layer_elems;
       GemmArgs q{};
-      q.M = M; q.A = c->a_n; q.a_plane = MA * d; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
+      q.M = M; q.A = c->a_n; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
       norm_fields(q); q.use_rstd = 1;
@@ -576,18 +593,18 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       at.kc = kc; at.vtc = vtc;
       UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s, ea_, eb_));
       GemmArgs o{};
-      o.M = M; o.A = c->a_o; o.a_plane = MA * c->q_dim; o.W = lp.wo; o.N = d; o.K = c->q_dim;
+      o.M = M; o.A = c->a_o; o.W = lp.wo; o.N = d; o.K = c->q_dim;
       o.out = c->h; o.ldo = d; norm_fields(o);
-      o.gain_next = lp.mlp_norm; o.next = c->a_n; o.next_plane = MA * d;
+      o.gain_next = lp.mlp_norm; o.next = c->a_n;
       UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, po, s, ea_, eb_));
       GemmArgs gu{};
-      gu.M = M; gu.A = c->a_n; gu.a_plane = MA * d; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
-      gu.out = c->a_g; gu.ldo = F; gu.out_plane = MA * F; norm_fields(gu); gu.use_rstd = 1;
-      UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU_BF16, gu, pg, s, ea_, eb_));
+      gu.M = M; gu.A = c->a_n; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
+      gu.out = c->a_g; gu.ldo = F; norm_fields(gu); gu.use_rstd = 1;
+      UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU, gu, pg, s, ea_, eb_));
       GemmArgs dn{};
-      dn.M = M; dn.A = c->a_g; dn.a_plane = MA * F; dn.W = lp.wdown; dn.N = d; dn.K = F;
+      dn.M = M; dn.A = c->a_g; dn.W = lp.wdown; dn.N = d; dn.K = F;
       dn.out = c->h; dn.ldo = d; norm_fields(dn);
-      dn.gain_next = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr; dn.next = c->a_n; dn.next_plane = MA * d;
+      dn.gain_next = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr; dn.next = c->a_n;
       UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_RESID_F32, dn, pd, s, ea_, eb_));
     }
   }

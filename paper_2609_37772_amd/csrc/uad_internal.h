@@ -25,31 +25,34 @@ namespace uad {
   } while (0)
 
 // ---------------------------------------------------------------------------
-// Vector types for the gfx950 bf16 MFMA builtins
+// Vector types for the gfx950 MFMA builtins
 // ---------------------------------------------------------------------------
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+// Projection operands (weights and activations) are fp16.  The model's
+// weights are bf16 values and fp16 holds every bf16 value of magnitude in
+// [2^-14, 65504] exactly (8 significant bits fit in 11), so the weight stream
+// is the bf16 model itself; smaller magnitudes round to the nearest fp16
+// subnormal (absolute error <= 2^-25) and larger ones are rejected at load.
+// Activations keep 11 significant bits instead of bf16's 8, which keeps the
+// rounding accumulated over the layer stack and the Euler steps well inside
+// the velocity tolerance while each activation costs 2 bytes to stream.
+typedef _Float16 op_t;
 
 // Packed weight layout used by every MFMA GEMM ("fragment order"):
 // a row-major W[N][K] (PyTorch [out][in]) is cut into 16x32 blocks; block
-// (nt, kb) holds 64 lanes x 8 consecutive-k bf16 values, lane l carrying
+// (nt, kb) holds 64 lanes x 8 consecutive-k fp16 values, lane l carrying
 // W[16*nt + (l & 15)][32*kb + 8*(l >> 4) + e], e = 0..7.  Blocks are stored
 // n-tile major, so one 16-column tile's whole K stream is contiguous and each
 // lane's operand is one aligned 16-byte load.
 constexpr int kTileN = 16;
 constexpr int kTileK = 32;
-constexpr int kBlockElems = kTileN * kTileK;  // 512 bf16 = 1 KiB
+constexpr int kBlockElems = kTileN * kTileK;  // 512 fp16 = 1 KiB
 
-// GEMM activation operands are carried as two bf16 planes, hi = bf16(a) and
-// lo = bf16(a - hi), stored `plane` elements apart; the GEMMs multiply both
-// planes by the same bf16 weight fragment.  This keeps ~16 significant bits
-// of every activation while the weights (bf16 by definition) are read once.
-__device__ __forceinline__ void store_split(__bf16 *hi, size_t plane, float v) {
-  const __bf16 h = (__bf16)v;
-  hi[0] = h;
-  hi[plane] = (__bf16)(v - (float)h);
-}
+__device__ __forceinline__ void store_op(op_t *p, float v) { *p = (op_t)v; }
 
 // Activation operands use the same fragment order as the weights: a
 // [rows][K] matrix (rows padded to 16) is stored as [rows/16][K/32][64][8],
@@ -63,9 +66,9 @@ __host__ __device__ __forceinline__ size_t afrag_index(int r, int c, int KB) {
 // Kernel argument blocks
 // ---------------------------------------------------------------------------
 enum Epilogue : int {
-  EPI_BIAS_SILU_BF16 = 0,  // out = split bf16 planes of silu(acc + bias), fragment order
-  EPI_RESID_F32 = 1,       // h = (bias | h) + acc; per-tile sum of squares; next operand split(h * gain_next)
-  EPI_GEGLU_BF16 = 3,      // out = split planes of gelu_tanh(rstd*acc_gate) * rstd*acc_up (interleaved gate/up)
+  EPI_BIAS_SILU = 0,   // out = fp16 silu(acc + bias), fragment order
+  EPI_RESID_F32 = 1,   // h = (bias | h) + acc; per-tile sum of squares; next operand fp16(h * gain_next)
+  EPI_GEGLU = 3,       // out = fp16 gelu_tanh(rstd*acc_gate) * rstd*acc_up (interleaved gate/up)
   EPI_QKV = 4,             // rstd*acc: q -> bf16 q buffer; k, v -> per-layer K / V^T store
 };
 
@@ -79,21 +82,17 @@ struct GemmPlan {
 };
 
 struct GemmArgs {
-  const __bf16 *A;  // activations, hi plane, fragment order [rows/16][K/32][64][8]
-  int lda;
-  size_t a_plane;   // element offset of the lo plane
-  size_t out_plane; // element offset of the lo plane of a split bf16 output
+  const op_t *A;    // activations, fragment order [rows/16][K/32][64][8]
   // RMSNorm folded into the GEMMs: a residual GEMM writes ssq[tile][row] (sum of
-  // squares of h over its 16 columns) and the next operand split(h * gain_next);
+  // squares of h over its 16 columns) and the next operand fp16(h * gain_next);
   // a consuming GEMM scales its accumulator by rstd[row] from those sums.
   float *ssq;             // [d/16][m_alloc]
   int ssq_tiles, m_alloc;
   float eps;
   const float *gain_next; // EPI_RESID_F32: gain of the following RMSNorm (nullptr: none)
-  __bf16 *next;           // EPI_RESID_F32: next operand, split planes, fragment order (K = N)
-  size_t next_plane;
-  int use_rstd;           // EPI_QKV / EPI_GEGLU_BF16: scale by rstd from ssq
-  const __bf16 *W;  // packed weights, N/16 tiles x K/32 blocks
+  op_t *next;             // EPI_RESID_F32: next operand, fragment order (K = N)
+  int use_rstd;           // EPI_QKV / EPI_GEGLU: scale by rstd from ssq
+  const op_t *W;    // packed weights, N/16 tiles x K/32 blocks
   int M, N, K;      // N counts packed output columns (2F for gate/up)
   void *out;        // epilogue destination
   int ldo;          // its row length (= K of the consuming GEMM for fragment-order outputs)
@@ -114,9 +113,8 @@ struct AttnArgs {
   int chunk, n_heads, n_kv_heads, group, rows, rows_pad;
   int splits, blocks_per_split;
   float scale_log2;  // log2(e) / sqrt(hd)
-  __bf16 *o;         // [M][ldo] bf16, hi plane (lo plane o_plane elements further)
+  op_t *o;           // O-projection operand, fragment order, K = ldo
   int ldo;
-  size_t o_plane;
   float *opart;      // [splits][B*Hkv][rows_pad][hd] (splits > 1)
   float *mlpart;     // [splits][B*Hkv][rows_pad][2]
 };
@@ -152,7 +150,7 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
 hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0 = nullptr,
                             hipEvent_t ev1 = nullptr);
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
-                       const float *b_in, const float *freqs, __bf16 *te, size_t plane, hipStream_t s,
+                       const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
@@ -185,7 +183,7 @@ struct GraphKey {
 };
 
 struct uad_layer_ptrs {
-  const __bf16 *wqkv, *wo, *wgu, *wdown;
+  const uad::op_t *wqkv, *wo, *wgu, *wdown;
   const float *attn_norm, *mlp_norm;
 };
 
@@ -198,7 +196,7 @@ struct uad_ctx {
 
   int d = 0, L = 0, Hq = 0, Hkv = 0, hd = 0, F = 0, Da = 0;
   int q_dim = 0, kv_dim = 0, n_qkv = 0;
-  int m_alloc = 0;   // activation rows, multiple of 64 (split buffers: 2 planes of m_alloc rows)
+  int m_alloc = 0;   // activation rows, multiple of 64
   int s_alloc = 0;   // key slots per (layer, env, kv head), multiple of 32
 
   // weights
@@ -206,7 +204,7 @@ struct uad_ctx {
   size_t wbytes = 0;
   float *action_in_w = nullptr, *action_in_b = nullptr, *t1_b = nullptr, *t2_b = nullptr;
   float *final_norm = nullptr, *action_out_w = nullptr, *action_out_b = nullptr, *freqs = nullptr;
-  __bf16 *t1_w = nullptr, *t2_w = nullptr;
+  uad::op_t *t1_w = nullptr, *t2_w = nullptr;
   std::vector<uad_layer_ptrs> layers;
   bool weights_loaded = false;
 
@@ -218,7 +216,8 @@ struct uad_ctx {
 
   // activation workspace
   float *h = nullptr;
-  __bf16 *a_te = nullptr, *a_z = nullptr, *a_n = nullptr, *a_o = nullptr, *a_g = nullptr, *q = nullptr;
+  uad::op_t *a_te = nullptr, *a_z = nullptr, *a_n = nullptr, *a_o = nullptr, *a_g = nullptr;
+  __bf16 *q = nullptr;
   float *attn_opart = nullptr, *attn_ml = nullptr;
   size_t attn_part_elems = 0;
   float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]

@@ -226,3 +226,24 @@ def test_batch_subset_matches_full_batch(gpu):
     _, v3 = gpu_velocity(c, c.noise, t[2], dt[2], mask[2])
     _, v1 = gpu_velocity(c, c.noise[:1], t[2][:1], dt[2][:1], mask[2][:1])
     assert rel_err(v1[0], v3[0]) <= 1e-3
+
+
+@pytest.mark.gpu
+def test_weight_beyond_fp16_range_is_rejected(gpu):
+    """Projection weights are held as fp16 (exact for bf16 magnitudes in
+    [2^-14, 65504]); a weight outside that range must be refused, not
+    silently turned into inf."""
+    import paper_2609_37772_amd as U
+    case = make_case("tiny", with_expert=False)
+    ex = U.ActionExpert(case.wl.shape, 1, case.wl.chunk, case.wl.prefix)
+    try:
+        bad = dict(case.weights)
+        w = bad["layers.0.w_up"].copy()
+        w[3, 5] = 1.0e5
+        bad["layers.0.w_up"] = w
+        with pytest.raises(U.UadError) as ei:
+            ex.load_weights(bad)
+        assert "fp16" in str(ei.value)
+        ex.load_weights(case.weights)  # the same context accepts in-range weights afterwards
+    finally:
+        ex.close()
