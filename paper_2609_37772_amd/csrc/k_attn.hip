@@ -7,30 +7,58 @@
 //
 // Per workgroup: one (environment, KV head), 64 packed query rows (4 waves x
 // 16), and a contiguous range of 32-key blocks (split-KV when the batch is
-// small).  K and V^T blocks are staged in LDS and shared by the 4 waves; the
-// next block's global loads are issued before the current block is used.
+// small).  Keys are processed in chunks of NB blocks: a chunk's K and V^T
+// tiles go straight from global memory into LDS (LDS-direct loads, shared by
+// the 4 waves, double buffered), all issued at once, and the next chunk's
+// loads are in flight while a chunk is used, so a split of at most NB blocks
+// costs one memory round trip.
 // Each wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 so that a
 // lane ends up holding 8 scores of ONE query, which are exactly the 8 k-values
 // of its operand for the P V product: no transpose through LDS.  Softmax
 // statistics are reduced across the 4 lanes that share a query with
-// wavefront shuffles (online softmax, fp32, exp2 domain).  With split-KV the
+// wavefront shuffles (online softmax, fp32, exp2 domain, accumulators
+// rescaled only when the running max moves by more than 2^8).  With split-KV the
 // unnormalised partial outputs and (max, sum) pairs are merged in fixed split
 // order by attn_combine_kernel.
 #include "uad_internal.h"
 
 namespace uad {
 
+// One 32-key block in LDS, filled by LDS-direct global loads (16 bytes per
+// lane, lane-linear placement) and read as MFMA fragments.  Rows are stored
+// unpadded with their 16-byte chunks XOR-swizzled so that the 8 lanes served
+// per LDS cycle hit distinct banks:
+//   K:   32 keys x HD,  chunk j of key row r stored at chunk j ^ (r & 7);
+//   V^T: HD x 32 keys (permuted, see vt_index), chunk g of column row c
+//        stored at chunk g ^ ((c >> 1) & 3).
 template <int HD>
-struct AttnSmem {
-  __bf16 k[32][HD + 8];   // 32 keys x HD (+16 B pad: conflict-free 16 B reads)
-  __bf16 vt[HD][32 + 4];  // HD x 32 keys (+8 B pad: conflict-free 8 B reads)
+struct AttnBlock {
+  __bf16 k[32 * HD];
+  __bf16 vt[HD * 32];
 };
 
+// Softmax rescaling threshold (log2 domain): the running max of a query is
+// only raised when a block's max exceeds it by more than this, so most blocks
+// skip rescaling the accumulators; probabilities stay <= 2^8.
+constexpr float kRescaleThreshold = 8.0f;
+
+// Blocks per chunk (one memory round trip); two chunks are resident (double
+// buffer), 2 * NB * 32 * HD * 4 bytes of LDS.
 template <int HD>
+constexpr int attn_chunk_blocks() {
+  return HD == 256 ? 2 : 4;
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int HD, int NB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
-  __shared__ AttnSmem<HD> sm;
-  constexpr int KS = HD / 32;  // k-steps of the QK^T product
-  constexpr int NTO = HD / 16; // 16-column output tiles
+  extern __shared__ __align__(16) unsigned char attn_smem[];
+  AttnBlock<HD> *bufs = (AttnBlock<HD> *)attn_smem;  // [2][NB]
+  constexpr int KS = HD / 32;   // k-steps of the QK^T product
+  constexpr int NTO = HD / 16;  // 16-column output tiles
+  constexpr int CPR = HD / 8;   // 16-byte chunks per K row
+  constexpr int INS = HD / 64;  // LDS-direct instructions per wave per tile (4 waves x 64 lanes x 16 B)
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int qblock = blockIdx.x;
@@ -40,9 +68,14 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int g = eh - b * a.n_kv_heads;
 
   const __bf16 *kbase = a.kc + (size_t)eh * a.s_alloc * HD;
-  const __bf16 *vbase = a.vtc + (size_t)eh * HD * a.s_alloc;
+  const __bf16 *vbase = a.vtc + vt_index(eh, 0, 0, HD, a.s_alloc);
 
-  // This lane's query (as the B operand of S^T) : packed row r0 + (lane & 15)
+  const int n_blocks = (a.n_keys + 31) / 32;
+  const int blk0 = split * a.blocks_per_split;
+  int blk1 = blk0 + a.blocks_per_split;
+  if (blk1 > n_blocks) blk1 = n_blocks;
+
+  // This lane's query (as the B operand of S^T): packed row r0 + (lane & 15).
   const int r0 = qblock * 64 + wave * 16;
   const int my_r = r0 + (lane & 15);
   bf16x8 qf[KS];
@@ -53,121 +86,112 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int head = g * a.group + hg;
     const __bf16 *qp = a.q + (size_t)(b * a.chunk + tok) * a.ldq + head * HD + (lane >> 4) * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ok)
-        qf[ks] = *(const bf16x8 *)(qp + ks * 32);
-      else
-        qf[ks] = bf16x8{};
-    }
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = ok ? *(const bf16x8 *)(qp + ks * 32) : bf16x8{};
   }
+
+  // LDS-direct loads of the chunk starting at block c0 into buffer set `which`
+  // (blocks past the split's end re-read its last block; never used).
+  auto issue = [&](int c0, int which) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int blk = min(c0 + j, blk1 - 1);
+      AttnBlock<HD> &dst = bufs[which * NB + j];
+      const __bf16 *kb = kbase + (size_t)blk * 32 * HD;
+      const __bf16 *vb = vbase + (size_t)blk * 32 * HD;
+#pragma unroll
+      for (int i = 0; i < INS; ++i) {
+        const int q0 = (wave * INS + i) * 64;  // first LDS chunk of this instruction
+        const int q = q0 + lane;
+        const int kr = q / CPR, kp = q - kr * CPR;
+        __builtin_amdgcn_global_load_lds((const void *)(kb + kr * HD + ((kp ^ (kr & 7)) * 8)),
+                                         (lds_void *)(dst.k + q0 * 8), 16, 0, 0);
+        const int vr = q >> 2, vp = q & 3;
+        __builtin_amdgcn_global_load_lds((const void *)(vb + vr * 32 + ((vp ^ ((vr >> 1) & 3)) * 8)),
+                                         (lds_void *)(dst.vt + q0 * 8), 16, 0, 0);
+      }
+    }
+  };
+  if (blk0 < blk1) issue(blk0, 0);
 
   f32x4 o[NTO];
 #pragma unroll
   for (int nt = 0; nt < NTO; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY;  // running max (log2 domain) of query (lane & 15)
+  float m_run = -INFINITY;  // reference max (log2 domain) of query (lane & 15), within 2^8 of the true max
   float l_run = 0.f;        // this lane's partial sum of exp2
 
-  const int n_blocks = (a.n_keys + 31) / 32;
-  const int blk0 = split * a.blocks_per_split;
-  int blk1 = blk0 + a.blocks_per_split;
-  if (blk1 > n_blocks) blk1 = n_blocks;
+  int which = 0;
+  for (int c0 = blk0; c0 < blk1; c0 += NB, which ^= 1) {
+    const int nb = min(NB, blk1 - c0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this chunk's LDS-direct loads (and q) landed
+    __syncthreads();  // ... for every wave; the other buffer set is free again
+    if (c0 + NB < blk1) issue(c0 + NB, which ^ 1);
 
-  // K/V blocks are prefetched into registers one block ahead, so the global
-  // loads of block b+1 are in flight while block b is multiplied from LDS.
-  constexpr int KCH = 32 * HD / 8 / 256;  // 16-byte K chunks per thread
-  constexpr int VCH = HD * 4 / 256;       // 16-byte V^T chunks per thread
-  bf16x8 kreg[KCH], vreg[VCH];
-  auto fetch = [&](int blk) {
-    const int k0 = blk * 32;
+#pragma nounroll
+    for (int j = 0; j < nb; ++j) {
+      const AttnBlock<HD> &blk = bufs[which * NB + j];
+      const int k0 = (c0 + j) * 32;
+      // S^T for two 16-key halves: s[h][r] = score(query lane&15, key k0+16h+4(lane>>4)+r).
+      // All K and V fragments of the block are read up front.
+      bf16x8 kf[2][KS], vf[NTO];
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = c / (HD / 8), col = (c - row * (HD / 8)) * 8;
-      kreg[i] = *(const bf16x8 *)(kbase + (size_t)(k0 + row) * HD + col);
-    }
+      for (int h = 0; h < 2; ++h) {
+        const int row = 16 * h + (lane & 15);
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = c >> 2, col = (c & 3) * 8;
-      vreg[i] = *(const bf16x8 *)(vbase + (size_t)row * a.s_alloc + k0 + col);
-    }
-  };
-  if (blk0 < blk1) fetch(blk0);
-
-  for (int blk = blk0; blk < blk1; ++blk) {
-    const int k0 = blk * 32;
-    __syncthreads();  // previous block fully consumed
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = c / (HD / 8), col = (c - row * (HD / 8)) * 8;
-      *(bf16x8 *)&sm.k[row][col] = kreg[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = c >> 2, col = (c & 3) * 8;
-      const bf16x8 v = vreg[i];
-      *(bf16x4 *)&sm.vt[row][col] = bf16x4{v[0], v[1], v[2], v[3]};
-      *(bf16x4 *)&sm.vt[row][col + 4] = bf16x4{v[4], v[5], v[6], v[7]};
-    }
-    __syncthreads();
-    if (blk + 1 < blk1) fetch(blk + 1);
-
-    // S^T for two 16-key halves: s[h][r] = score(query lane&15, key k0+16h+4(lane>>4)+r)
-    f32x4 s[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      s[h] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 kf = *(const bf16x8 *)&sm.k[16 * h + (lane & 15)][ks * 32 + (lane >> 4) * 8];
-        s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[h], 0, 0, 0);
+        for (int ks = 0; ks < KS; ++ks)
+          kf[h][ks] = *(const bf16x8 *)&blk.k[row * HD + (((ks * 4 + (lane >> 4)) ^ (row & 7)) * 8)];
       }
-    }
-    float mloc = -INFINITY;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + 16 * h + (lane >> 4) * 4 + r;
-        float v = s[h][r] * a.scale_log2;
-        if (key >= a.n_keys) v = -INFINITY;
-        s[h][r] = v;
-        mloc = fmaxf(mloc, v);
+      for (int nt = 0; nt < NTO; ++nt) {
+        const int c = nt * 16 + (lane & 15);
+        vf[nt] = *(const bf16x8 *)&blk.vt[c * 32 + (((lane >> 4) ^ ((c >> 1) & 3)) * 8)];
       }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, mloc);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-    bf16x8 pf;
+      f32x4 s[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(s[h][r] - m_new);
-        psum += p;
-        pf[h * 4 + r] = (__bf16)p;
+        for (int h = 0; h < 2; ++h) s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[h][ks], qf[ks], s[h], 0, 0, 0);
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = k0 + 16 * h + (lane >> 4) * 4 + r;
+          float v = s[h][r] * a.scale_log2;
+          if (key >= a.n_keys) v = -INFINITY;
+          s[h][r] = v;
+          mloc = fmaxf(mloc, v);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      // lazy rescale: raise the running max only past the threshold (whole wave)
+      if (__any(mloc > m_run + kRescaleThreshold)) {
+        const float m_new = fmaxf(m_run, mloc);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // arguments <= 0
+        m_run = m_new;
+        l_run *= alpha;
+        // output rows (row 4*(lane>>4)+r of the tile) take their query's alpha
+        float al[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, (lane >> 4) * 4 + r);
+#pragma unroll
+        for (int nt = 0; nt < NTO; ++nt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[nt][r] *= al[r];
       }
-    l_run = l_run * alpha + psum;
-    // rescale output rows (row 4*(lane>>4)+r of the tile) by their query's alpha
-    float al[4];
+      float psum = 0.f;
+      bf16x8 pf;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, (lane >> 4) * 4 + r);
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int nt = 0; nt < NTO; ++nt)
+        for (int r = 0; r < 4; ++r) {
+          const float p = __builtin_amdgcn_exp2f(s[h][r] - m_run);
+          psum += p;
+          pf[h * 4 + r] = (__bf16)p;
+        }
+      l_run += psum;
+      // O += P V : B operand lane l = V[keys of pf][col 16nt + (l&15)]
 #pragma unroll
-      for (int r = 0; r < 4; ++r) o[nt][r] *= al[r];
-    // O += P V : B operand lane l = V[keys of pf][col 16nt + (l&15)]
-#pragma unroll
-    for (int nt = 0; nt < NTO; ++nt) {
-      const __bf16 *vr = &sm.vt[nt * 16 + (lane & 15)][0];
-      const bf16x4 v0 = *(const bf16x4 *)(vr + (lane >> 4) * 4);
-      const bf16x4 v1 = *(const bf16x4 *)(vr + 16 + (lane >> 4) * 4);
-      const bf16x8 vf = bf16x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-      o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf, o[nt], 0, 0, 0);
+      for (int nt = 0; nt < NTO; ++nt) o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf[nt], o[nt], 0, 0, 0);
     }
   }
 
@@ -175,14 +199,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   l_tot += __shfl_xor(l_tot, 16);
   l_tot += __shfl_xor(l_tot, 32);
 
-  // Output rows of this lane: r0 + 4*(lane>>4) + r, column 16*nt + (lane&15)
-  float lr[4], mr[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    lr[r] = __shfl(l_tot, (lane >> 4) * 4 + r);
-    mr[r] = __shfl(m_run, (lane >> 4) * 4 + r);
-  }
   if (a.splits == 1) {
+    // Output rows of this lane: r0 + 4*(lane>>4) + r, column 16*nt + (lane&15)
+    float lr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) lr[r] = __shfl(l_tot, (lane >> 4) * 4 + r);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = r0 + (lane >> 4) * 4 + r;
@@ -196,71 +217,113 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv);
     }
   } else {
-    const size_t pbase = ((size_t)split * gridDim.z + eh) * a.rows_pad;
+    // Partials in the accumulator's own layout: per 16-row tile, [nt][lane][4]
+    // floats (one 16-byte store per lane and column tile), and (m, l) per row.
+    const size_t tile = ((size_t)split * gridDim.z + eh) * (a.rows_pad / 16) + (r0 >> 4);
+    float *op = a.opart + tile * (16 * HD) + lane * 4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = r0 + (lane >> 4) * 4 + r;
-      if (row >= a.rows) continue;
-      float *op = a.opart + (pbase + row) * HD + (lane & 15);
-#pragma unroll
-      for (int nt = 0; nt < NTO; ++nt) op[nt * 16] = o[nt][r];
-      if ((lane & 15) == 0) {
-        a.mlpart[(pbase + row) * 2 + 0] = mr[r];
-        a.mlpart[(pbase + row) * 2 + 1] = lr[r];
-      }
-    }
+    for (int nt = 0; nt < NTO; ++nt) *(f32x4 *)(op + nt * 256) = o[nt];
+    // lanes 0..15 hold the statistics of their own query row r0 + lane
+    if (lane < 16) *(float2 *)(a.mlpart + (tile * 16 + lane) * 2) = float2{m_run, l_tot};
   }
 }
 
 // Merge split-KV partials: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
-// splits in fixed order.  The (m_s, l_s) pairs of the row are staged in LDS
-// by one vector load per thread; every partial load is issued up front.
-constexpr int kMaxKvSplits = 32;
-template <int HD>
-__global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a) {
-  __shared__ float2 mls[kMaxKvSplits];
-  const int row = blockIdx.x;
-  const int eh = blockIdx.y;
+// splits in fixed order.  One wave per (16-row tile, 16-column tile): lane l
+// owns the float4 of the accumulator layout (rows 4*(l>>4)..+3, column l&15)
+// and reads the (m, l) pairs of its 4 rows itself, so all loads are issued
+// up front and the merge needs no LDS or barrier.
+template <int SMAX>
+__global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
+  const int rt = blockIdx.x;  // 16-row tile
+  const int nt = blockIdx.y;  // 16-column tile
+  const int eh = blockIdx.z;
   const int b = eh / a.n_kv_heads, g = eh - b * a.n_kv_heads;
-  const int c = threadIdx.x;
-  const int n_eh = gridDim.y;
+  const int n_eh = gridDim.z;
   const int splits = a.splits;
-  const float *__restrict__ opart = a.opart;
-  if (c < kMaxKvSplits)
-    mls[c] = c < splits ? *(const float2 *)(a.mlpart + (((size_t)c * n_eh + eh) * a.rows_pad + row) * 2)
-                        : float2{-INFINITY, 0.f};
-  float os[kMaxKvSplits];
+  const int ntiles = a.rows_pad / 16;
+  const int lane = threadIdx.x;
+  const int rbase = (lane >> 4) * 4;
+  f32x4 os[SMAX];
+  float2 ml[SMAX][4];
 #pragma unroll
-  for (int s = 0; s < kMaxKvSplits; ++s)
-    os[s] = s < splits ? opart[(((size_t)s * n_eh + eh) * a.rows_pad + row) * HD + c] : 0.f;
-  __syncthreads();
-  float M = -INFINITY;
+  for (int sp = 0; sp < SMAX; ++sp) {
+    const size_t tile = ((size_t)min(sp, splits - 1) * n_eh + eh) * ntiles + rt;
+    const f32x4 ov = *(const f32x4 *)(a.opart + tile * (16 * (size_t)hd) + nt * 256 + lane * 4);
+    os[sp] = sp < splits ? ov : f32x4{};
 #pragma unroll
-  for (int s = 0; s < kMaxKvSplits; ++s) M = fmaxf(M, mls[s].x);
-  float num = 0.f, den = 0.f;
-#pragma unroll
-  for (int s = 0; s < kMaxKvSplits; ++s) {
-    if (s < splits) {
-      const float w = exp2f(mls[s].x - M);
-      num += w * os[s];
-      den += w * mls[s].y;
+    for (int r = 0; r < 4; ++r) {
+      const float2 v = *(const float2 *)(a.mlpart + (tile * 16 + rbase + r) * 2);
+      ml[sp][r] = sp < splits ? v : float2{-INFINITY, 0.f};
     }
   }
-  const int hg = row / a.chunk, tok = row - hg * a.chunk;
-  const int head = g * a.group + hg;
-  store_op(a.o + afrag_index(b * a.chunk + tok, head * HD + c, a.ldo / kTileK), num / den);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp) M = fmaxf(M, ml[sp][r].x);
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp) {
+      const float w = sp < splits ? __builtin_amdgcn_exp2f(ml[sp][r].x - M) : 0.f;
+      num += w * os[sp][r];
+      den += w * ml[sp][r].y;
+    }
+    const int row = rt * 16 + rbase + r;
+    if (row >= a.rows) continue;
+    const int hg = row / a.chunk, tok = row - hg * a.chunk;
+    const int head = g * a.group + hg;
+    store_op(a.o + afrag_index(b * a.chunk + tok, head * hd + nt * 16 + (lane & 15), a.ldo / kTileK), num / den);
+  }
 }
 
 template <int HD>
 static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  constexpr int NB = attn_chunk_blocks<HD>();
   dim3 grid((a.rows + 63) / 64, a.splits, batch * a.n_kv_heads);
   hipEvent_t end_attn = a.splits == 1 ? ev1 : nullptr;
-  UAD_LAUNCH((attn_kernel<HD>), grid, dim3(256), 0, s, ev0, end_attn, a);
+  const uint32_t lds = (uint32_t)(2 * NB * sizeof(AttnBlock<HD>));
+  UAD_LAUNCH((attn_kernel<HD, NB>), grid, dim3(256), lds, s, ev0, end_attn, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   hipEvent_t none = nullptr;
-  UAD_LAUNCH((attn_combine_kernel<HD>), dim3(a.rows, batch * a.n_kv_heads), dim3(HD), 0, s, none, ev1, a);
+  const dim3 cgrid(a.rows_pad / 16, HD / 16, batch * a.n_kv_heads);
+  if (a.splits <= 4)
+    UAD_LAUNCH((attn_combine_kernel<4>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+  else if (a.splits <= 8)
+    UAD_LAUNCH((attn_combine_kernel<8>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+  else if (a.splits <= 16)
+    UAD_LAUNCH((attn_combine_kernel<16>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+  else if (a.splits <= 32)
+    UAD_LAUNCH((attn_combine_kernel<32>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+template <int HD>
+static hipError_t init_hd() {
+  constexpr int NB = attn_chunk_blocks<HD>();
+  return hipFuncSetAttribute((const void *)attn_kernel<HD, NB>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)(2 * NB * sizeof(AttnBlock<HD>)));
+}
+
+hipError_t attention_init() {
+  hipError_t e = init_hd<64>();
+  if (e == hipSuccess) e = init_hd<128>();
+  if (e == hipSuccess) e = init_hd<256>();
+  return e;
+}
+
+int attention_max_splits(int) { return 32; }
+
+int attention_chunk_blocks(int head_dim) {
+  switch (head_dim) {
+    case 64: return attn_chunk_blocks<64>();
+    case 128: return attn_chunk_blocks<128>();
+    case 256: return attn_chunk_blocks<256>();
+  }
+  return 1;
 }
 
 hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0,

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
           if (!is_v)
             g.kc[(env_head * g.s_alloc + s) * g.head_dim + c] = (__bf16)v;
           else
-            g.vtc[(env_head * g.head_dim + c) * g.s_alloc + s] = (__bf16)v;
+            g.vtc[vt_index(env_head, s, c, g.head_dim, g.s_alloc)] = (__bf16)v;
         }
       }
     }

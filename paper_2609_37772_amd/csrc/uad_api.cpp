@@ -127,13 +127,15 @@ int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) {
   const int rows = (c->Hq / c->Hkv) * H;
   const int qblocks = (rows + 63) / 64;
   const int n_blocks = (P + H + 31) / 32;
-  // split the keys until the grid covers the chip, at >= 2 key blocks per split
   const int wgs = qblocks * B * c->Hkv;
-  const int want = (256 + wgs - 1) / wgs;
-  int per = (n_blocks + want - 1) / want;
-  if (per < 2) per = 2;
-  if ((n_blocks + per - 1) / per > 32) per = (n_blocks + 31) / 32;  // combine handles <= 32 splits
-  if (per > n_blocks) per = n_blocks;
+  int per = n_blocks;
+  if (wgs < 128) {
+    // small batch: split the keys so each split is one chunk (one memory round trip)
+    per = attention_chunk_blocks(c->hd);
+    const int smax = attention_max_splits(c->hd);
+    if ((n_blocks + per - 1) / per > smax) per = (n_blocks + smax - 1) / smax;
+    if (per > n_blocks) per = n_blocks;
+  }
   *bps = per;
   return (n_blocks + per - 1) / per;
 }
@@ -251,7 +253,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
     }
   }
 
-  // K / V^T store: [L][max_batch][Hkv][s_alloc][hd] and [L][max_batch][Hkv][hd][s_alloc]
+  // K / V^T store: [L][max_batch][Hkv][s_alloc][hd] and [L][max_batch][Hkv][s_alloc/32][hd][32]
   c->kv_layer_elems = (size_t)m.max_batch * c->Hkv * c->s_alloc * c->hd;
   const size_t kv_bytes = c->kv_layer_elems * c->L * 2;
   e = hipMalloc((void **)&c->kcache, kv_bytes);
@@ -300,6 +302,11 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->attn_opart = (float *)(ab + o_op);
   c->attn_ml = (float *)(ab + o_ml);
   c->ssq = (float *)(ab + o_ssq);
+  e = attention_init();
+  if (e != hipSuccess) {
+    uad_destroy(c);
+    return cerr(UAD_E_HIP, std::string("attention kernel set-up: ") + hipGetErrorString(e));
+  }
   e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
   if (e != hipSuccess) {
     uad_destroy(c);
@@ -498,7 +505,7 @@ uad_status uad_set_prefix_kv(uad_ctx *c, const void *k, const void *v, int32_t d
             const size_t src = (((size_t)b * P + s) * Hkv + g) * hd + cc;
             const size_t eh = (size_t)b * Hkv + g;
             ks[(eh * S + s) * hd + cc] = f32_to_bf16_rne(kf[src]);
-            vs[(eh * hd + cc) * S + s] = f32_to_bf16_rne(vf[src]);
+            vs[vt_index(eh, s, cc, hd, S)] = f32_to_bf16_rne(vf[src]);
           }
     hipError_t e = hipMemcpy(c->kcache + l * c->kv_layer_elems, ks.data(), ks.size() * 2, hipMemcpyHostToDevice);
     if (e == hipSuccess)

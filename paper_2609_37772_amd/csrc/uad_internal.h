@@ -62,6 +62,18 @@ __host__ __device__ __forceinline__ size_t afrag_index(int r, int c, int KB) {
   return ((size_t)((r >> 4) * KB + (c >> 5)) * 64 + (r & 15) + 16 * ((c & 31) >> 3)) * 8 + (c & 7);
 }
 
+// K/V store layout per (layer, environment, KV head) with key slots padded to
+// s_alloc (a multiple of 32): K as [s_alloc][hd]; V transposed in 32-key
+// blocks, [s_alloc/32][hd][32], so one block's V^T tile is 32*hd contiguous
+// values.  Within a block the 32 keys of a V^T row are stored permuted: key
+// 16h + 4g + r (h < 2, g < 4, r < 4) at position 8g + 4h + r, the order in
+// which the attention kernel's P V operand consumes them (8 contiguous keys
+// per lane).  Index of V(key s, column c) of environment-head eh:
+__host__ __device__ __forceinline__ int vt_key_pos(int k) { return ((k >> 2) & 3) * 8 + (k >> 4) * 4 + (k & 3); }
+__host__ __device__ __forceinline__ size_t vt_index(size_t eh, int s, int c, int hd, int s_alloc) {
+  return eh * (size_t)hd * s_alloc + ((size_t)(s >> 5) * hd + c) * 32 + vt_key_pos(s & 31);
+}
+
 // ---------------------------------------------------------------------------
 // Kernel argument blocks
 // ---------------------------------------------------------------------------
@@ -99,7 +111,7 @@ struct GemmArgs {
   const float *bias;
   // EPI_QKV destinations
   __bf16 *kc;   // layer K store [B][Hkv][S_alloc][hd]
-  __bf16 *vtc;  // layer V^T store [B][Hkv][hd][S_alloc]
+  __bf16 *vtc;  // layer V^T store, 32-key blocks (vt_index)
   int chunk, prefix, s_alloc, n_kv_heads, head_dim, q_dim;
 };
 
@@ -149,6 +161,9 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
                        hipEvent_t ev1 = nullptr);
 hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0 = nullptr,
                             hipEvent_t ev1 = nullptr);
+hipError_t attention_init();             // once per context: raise the kernels' LDS limit
+int attention_chunk_blocks(int head_dim);  // 32-key blocks loaded per round trip
+int attention_max_splits(int head_dim);    // split-KV partials the combine accepts
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                        const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
