@@ -165,6 +165,48 @@ uad_status uad_denoise_schedule(uad_ctx *ctx, float *x, const float *t_sched, co
                                 const uint8_t *mask_sched, int32_t n_steps, int32_t batch, int32_t chunk,
                                 float *released, int32_t *release_step, uint64_t *step_ticks);
 
+/* Urgency-aware release of one chunk per environment (Sec. 4.2-4.4, App. C).
+ * Tokens i < U are urgent: they take K steps of size 1/K while the tail takes
+ * the canonical N* steps of 1/N*, all in ONE joint evaluation per step (N*
+ * evaluations in total, none extra).  After step K the urgent actions
+ * a^i = x_K^i are released; then, by mode:
+ *   UAD_RELEASE_UAER  plain early release: urgent tokens stay frozen (t = 0) as
+ *                     context for the remaining N* - K steps;
+ *   UAD_RELEASE_TR    Trajectory Reconciliation (Sec. 4.3 Eqs. 6-7): their
+ *                     states are rebuilt from the cached velocities,
+ *                     x'_K = x_0 + (1/N*) sum_{k<=K} v_k (flow-time convention
+ *                     of the integrator: dt* = -1/N*), and continue as ghost
+ *                     states at the tail's flow time 1 - k/N*; with K = 1 the
+ *                     tail and the ghosts reproduce the uniform N*-step
+ *                     schedule bit for bit.
+ * Ghost Action Correction (Sec. 4.4 Eqs. 8-9, TR only): with executed_out,
+ * E = sum_{i<U} (a'^i - a^i) over the ghost actions a'^i = x'^i_{N*}, and
+ * the executed chunk is a^0..a^{U-1} (released, unchanged) followed by
+ * x^i_{N*} + E/(S - U) for i = U .. S-1 on the dimensions gac_mask selects.
+ *   x             device fp32 [batch][chunk][Da]: x_0 in; final states out
+ *                 (ghost states x'_{N*} for i < U with TR, frozen x_K without)
+ *   U, K, N*, S   1 <= U < S <= chunk, 1 <= K < N* <= 64
+ *   urgent_out    device fp32 [batch][U][Da]: the released urgent actions
+ *   executed_out  device fp32 [batch][S][Da] or NULL (requires UAD_RELEASE_TR)
+ *   gac_mask      device uint8 [Da] or NULL: 1 = additive dimension corrected,
+ *                 0 = left as denoised (e.g. a gripper); NULL corrects all
+ *   urgent_host   pinned host fp32 [batch][U][Da] or NULL: receives a copy of
+ *                 the urgent actions on a separate release stream as soon as
+ *                 step K is done, while the tail keeps denoising on the
+ *                 context's stream (App. C, asynchronous execution)
+ *   release_event hipEvent_t or NULL: recorded when the urgent actions (and
+ *                 their host copy, if requested) are final; a controller waits
+ *                 on it instead of on the whole chunk
+ *   step_ticks    pinned host uint64 [N* + 1] or NULL, as uad_denoise_schedule
+ * Asynchronous like uad_denoise_schedule; caller buffers must outlive the
+ * work.  Errors: UAD_E_INVALID (null x/urgent_out, bad U, K, N* or S, bad mode, GAC
+ * without TR), UAD_E_SHAPE, UAD_E_STATE, UAD_E_HIP. */
+enum { UAD_RELEASE_UAER = 0, UAD_RELEASE_TR = 1 };
+uad_status uad_denoise_release(uad_ctx *ctx, float *x, int32_t batch, int32_t chunk, int32_t U, int32_t K,
+                               int32_t Nstar, int32_t S, int32_t mode, float *urgent_out, float *executed_out,
+                               const uint8_t *gac_mask, float *urgent_host, void *release_event,
+                               uint64_t *step_ticks);
+
 /* Build the per-step tables from integer budgets N_i (Sec. 4.2 Eq. 4): pure
  * host code, no context needed.  budgets: host int32 [batch][chunk], each in
  * 1..max_steps.  Outputs (host, caller-allocated, capacity max_steps slices):

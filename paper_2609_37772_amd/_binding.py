@@ -17,19 +17,21 @@ import torch  # loaded first on purpose: libuad then binds to PyTorch's HIP runt
 __all__ = [
     "LIB_PATH", "EXPORTED_SYMBOLS", "UadError", "load_library", "library_loaded",
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
-    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_build_schedule",
-    "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
+    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_denoise_release",
+    "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
     "uad_profile_enable", "uad_profile_read", "UAD_DTYPE_F32", "UAD_DTYPE_BF16", "STATUS_NAMES",
+    "UAD_RELEASE_UAER", "UAD_RELEASE_TR",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libuad.so")
 UAD_DTYPE_F32, UAD_DTYPE_BF16 = 0, 1
+UAD_RELEASE_UAER, UAD_RELEASE_TR = 0, 1
 STATUS_NAMES = {0: "UAD_OK", 1: "UAD_E_INVALID", 2: "UAD_E_SHAPE", 3: "UAD_E_STATE", 4: "UAD_E_MISSING",
                 5: "UAD_E_HIP", 6: "UAD_E_OOM", 7: "UAD_E_UNSUPPORTED"}
 EXPORTED_SYMBOLS = [
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
-    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_build_schedule",
-    "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
+    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_denoise_release",
+    "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
     "uad_profile_enable", "uad_profile_read",
 ]
 
@@ -73,6 +75,7 @@ def load_library() -> ctypes.CDLL:
         "uad_set_prefix_kv": ([P, P, P, I32, I32, I32, I32], I32),
         "uad_denoise_step": ([P, P, P, P, P, P, I32, I32], I32),
         "uad_denoise_schedule": ([P, P, P, P, P, I32, I32, I32, P, P, P], I32),
+        "uad_denoise_release": ([P, P, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P, P], I32),
         "uad_build_schedule": ([P, I32, I32, I32, P, P, P, P], I32),
         "uad_aal": ([P, I32, ctypes.c_double, P], I32),
         "uad_synchronize": ([P], I32),
@@ -244,6 +247,42 @@ def uad_denoise_schedule(ctx: int, x: torch.Tensor, t_sched: torch.Tensor, dt_sc
         tk = step_ticks.data_ptr()
     st = load_library().uad_denoise_schedule(ctx, *p, n, B, H, rel, rst, tk)
     _check(ctx, st, "uad_denoise_schedule")
+
+
+def uad_denoise_release(ctx: int, x: torch.Tensor, U: int, K: int, Nstar: int, S: int, mode: int,
+                        urgent: torch.Tensor, executed: Optional[torch.Tensor] = None,
+                        gac_mask: Optional[torch.Tensor] = None, urgent_host: Optional[torch.Tensor] = None,
+                        release_event: Optional["torch.cuda.Event"] = None,
+                        step_ticks: Optional[torch.Tensor] = None) -> None:
+    """Urgency-aware release of a chunk per environment (UAER or TR, GAC with ``executed``).
+
+    x [B][H][Da] device fp32 in/out; urgent [B][U][Da] device; executed [B][S][Da] device;
+    gac_mask [Da] device uint8; urgent_host [B][U][Da] pinned host fp32; release_event a
+    torch.cuda.Event recorded when the urgent actions are final; step_ticks pinned uint64 [N*+1].
+    """
+    B, H, Da = x.shape
+    px = _dev_ptr(x, torch.float32, (B, H, Da), "x")
+    pu = _dev_ptr(urgent, torch.float32, (B, U, Da), "urgent")
+    pe = _dev_ptr(executed, torch.float32, (B, S, Da), "executed")
+    pm = _dev_ptr(gac_mask, torch.uint8, (Da,), "gac_mask")
+    ph = None
+    if urgent_host is not None:
+        if urgent_host.is_cuda or not urgent_host.is_pinned() or urgent_host.dtype != torch.float32 \
+                or tuple(urgent_host.shape) != (B, U, Da):
+            raise ValueError("urgent_host must be a pinned host fp32 tensor [B][U][Da]")
+        ph = urgent_host.data_ptr()
+    ev = None
+    if release_event is not None:
+        release_event.record()  # materialise the event before handing its handle over
+        ev = release_event.cuda_event
+    tk = None
+    if step_ticks is not None:
+        if step_ticks.is_cuda or not step_ticks.is_pinned() or step_ticks.dtype != torch.uint64 \
+                or tuple(step_ticks.shape) != (Nstar + 1,):
+            raise ValueError("step_ticks must be a pinned host uint64 tensor of N*+1 entries")
+        tk = step_ticks.data_ptr()
+    st = load_library().uad_denoise_release(ctx, px, B, H, U, K, Nstar, S, mode, pu, pe, pm, ph, ev, tk)
+    _check(ctx, st, "uad_denoise_release")
 
 
 def uad_build_schedule(budgets: np.ndarray, max_steps: int = 64):

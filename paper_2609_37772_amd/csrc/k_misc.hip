@@ -109,12 +109,59 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
     const float xn = frozen ? xo : xo + dtm * v;
     f.x[idx] = xn;
     if (f.v_out) f.v_out[idx] = v;
+    if (f.vsum && (m % f.chunk) < f.vsum_tokens) f.vsum[idx] += v;
     const bool releasing = !frozen && (f.is_last_step || (f.next_mask && f.next_mask[m] != 0));
     if (releasing) {
       if (f.released) f.released[idx] = xn;
       if (f.release_step && a == 0) f.release_step[m] = f.step;
     }
   }
+}
+
+// Trajectory Reconciliation set-up: keep the initial noise x_0 and clear the
+// velocity sums of the urgent tokens.
+__global__ __launch_bounds__(256) void tr_init_kernel(TrArgs a) {
+  const int n = a.B * a.H * a.Da;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    a.x0[i] = a.x[i];
+    a.vsum[i] = 0.f;
+  }
+}
+
+// Release after step K (Sec. 4.2): the urgent actions a^i = x_K^i, i < U, are
+// copied out; with Trajectory Reconciliation (Sec. 4.3, Eq. 6) their internal
+// states are then re-integrated under the canonical step,
+// x'_K = x_0 + (1/N*) sum_k v_k, written in the flow-time convention of the
+// integrator (dt* = -1/N*) and in the same form as its Euler update, so that
+// with K = 1 the reconciled state equals the uniform schedule's x_1 bit for bit.
+__global__ __launch_bounds__(256) void tr_release_kernel(TrArgs a) {
+  const int n = a.B * a.U * a.Da;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    const int c = i % a.Da;
+    const int bu = i / a.Da;
+    const int b = bu / a.U, u = bu - b * a.U;
+    const size_t idx = ((size_t)b * a.H + u) * a.Da + c;
+    a.urgent[i] = a.x[idx];
+    if (a.reconcile) a.x[idx] = a.x0[idx] + a.dt_star * a.vsum[idx];
+  }
+}
+
+// Ghost Action Correction (Sec. 4.4): E = sum_{i<U} (a'^i - a^i) over the ghost
+// actions a'^i = x'^i_{N*} and released a^i (Eq. 8, summed in token order),
+// then a^i = x^i_{N*} + E / (S - U) for i = U .. S-1 on the corrected
+// dimensions (Eq. 9); executed[0..U) are the released actions unchanged.
+__global__ __launch_bounds__(64) void gac_kernel(TrArgs a) {
+  const int b = blockIdx.x;
+  const int c = threadIdx.x;
+  if (c >= a.Da) return;
+  const float *xb = a.x + (size_t)b * a.H * a.Da;
+  const float *ub = a.urgent + (size_t)b * a.U * a.Da;
+  float *eb = a.executed + (size_t)b * a.S * a.Da;
+  float E = 0.f;
+  for (int i = 0; i < a.U; ++i) E += xb[(size_t)i * a.Da + c] - ub[(size_t)i * a.Da + c];
+  const float shift = (a.gac_mask == nullptr || a.gac_mask[c] != 0) ? E / (float)(a.S - a.U) : 0.f;
+  for (int i = 0; i < a.U; ++i) eb[(size_t)i * a.Da + c] = ub[(size_t)i * a.Da + c];
+  for (int i = a.U; i < a.S; ++i) eb[(size_t)i * a.Da + c] = xb[(size_t)i * a.Da + c] + shift;
 }
 
 __global__ void stamp_kernel(uint64_t *dst) {
@@ -144,6 +191,24 @@ hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0, hipEv
     case 8: UAD_LAUNCH(final_kernel<8>, grid, dim3(256), 0, s, ev0, ev1, f); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_tr_init(const TrArgs &a, hipStream_t s) {
+  const int n = a.B * a.H * a.Da;
+  hipLaunchKernelGGL(tr_init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tr_release(const TrArgs &a, hipStream_t s) {
+  const int n = a.B * a.U * a.Da;
+  hipLaunchKernelGGL(tr_release_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gac(const TrArgs &a, hipStream_t s) {
+  if (a.Da > 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gac_kernel, dim3(a.B), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

@@ -3,6 +3,7 @@
 // of one joint denoising step.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -284,7 +285,9 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(M * 2 * d), o_z = a.take<uint16_t>(M * d),
          o_n = a.take<uint16_t>(M * d), o_o = a.take<uint16_t>(M * c->q_dim), o_g = a.take<uint16_t>(M * F),
          o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
-         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M);
+         o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M),
+         o_trx0 = a.take<float>(M * Da), o_trv = a.take<float>(M * Da), o_trt = a.take<float>(kMaxTrSteps * M),
+         o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -302,15 +305,22 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->attn_opart = (float *)(ab + o_op);
   c->attn_ml = (float *)(ab + o_ml);
   c->ssq = (float *)(ab + o_ssq);
+  c->tr_x0 = (float *)(ab + o_trx0);
+  c->tr_vsum = (float *)(ab + o_trv);
+  c->tr_t = (float *)(ab + o_trt);
+  c->tr_dt = (float *)(ab + o_trdt);
+  c->tr_mask = (uint8_t *)(ab + o_trm);
   e = attention_init();
   if (e != hipSuccess) {
     uad_destroy(c);
     return cerr(UAD_E_HIP, std::string("attention kernel set-up: ") + hipGetErrorString(e));
   }
   e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->rel_stream, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_rel, hipEventDisableTiming);
   if (e != hipSuccess) {
     uad_destroy(c);
-    return cerr(UAD_E_HIP, std::string("hipStreamCreate(capture): ") + hipGetErrorString(e));
+    return cerr(UAD_E_HIP, std::string("hipStreamCreate(capture/release): ") + hipGetErrorString(e));
   }
   *out = c;
   g_create_err.clear();
@@ -332,6 +342,11 @@ void uad_destroy(uad_ctx *c) {
   for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
   for (auto &ge : c->graphs) (void)hipGraphExecDestroy(ge.exec);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+  if (c->rel_stream) {
+    (void)hipStreamSynchronize(c->rel_stream);
+    (void)hipStreamDestroy(c->rel_stream);
+  }
+  if (c->ev_rel) (void)hipEventDestroy(c->ev_rel);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
 }
@@ -540,7 +555,8 @@ static uad_status check_step_args(uad_ctx *c, const void *x, const void *t, cons
 // final norm/projection/Euler.
 static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float *t, const float *dt,
                                const uint8_t *mask, const uint8_t *next_mask, int is_last, int step, float *v_out,
-                               float *released, int32_t *release_step, int B, int H) {
+                               float *released, int32_t *release_step, int B, int H, float *vsum = nullptr,
+                               int vsum_tokens = 0) {
   const int M = B * H, d = c->d, F = c->F;
   const size_t MA = c->m_alloc;
   hipError_t e = hipSuccess;
@@ -620,6 +636,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
   f.M = M; f.d = d; f.Da = c->Da; f.x = x; f.t = t; f.dt = dt; f.mask = mask; f.next_mask = next_mask;
   f.is_last_step = is_last; f.step = step; f.v_out = v_out; f.released = released; f.release_step = release_step;
   f.debug_field = c->dbg ? 1 : 0; f.dbg_alpha = c->dbg_alpha; f.dbg_beta = c->dbg_beta;
+  f.vsum = vsum; f.vsum_tokens = vsum_tokens; f.chunk = H;
   UAD_CHECK_CLS(K_FINAL, launch_final(f, s, ea_, eb_));
 #undef UAD_CHECK_CLS
   return UAD_OK;
@@ -646,6 +663,39 @@ static uad_status enqueue_schedule(uad_ctx *c, hipStream_t s, const GraphKey &k)
   return UAD_OK;
 }
 
+// The two phases of an urgency-aware release (Sec. 4.2-4.4) on stream s.
+// Phase 1: keep x_0, steps 0 .. K-1 (urgent tokens on step 1/K, velocity sums
+// kept for TR), then release the urgent actions and reconcile their states.
+// Phase 2: steps K .. N*-1, then Ghost Action Correction of the tail.
+static uad_status enqueue_release_phase(uad_ctx *c, hipStream_t s, const GraphKey &k) {
+  const size_t M = (size_t)k.B * k.H;
+  TrArgs a{};
+  a.x = k.x; a.x0 = c->tr_x0; a.vsum = c->tr_vsum; a.urgent = k.urgent; a.executed = k.executed;
+  a.gac_mask = k.gac_mask; a.B = k.B; a.H = k.H; a.Da = c->Da; a.U = k.U; a.S = k.S;
+  a.dt_star = -(1.0f / (float)k.Nstar); a.reconcile = k.reconcile;
+  hipError_t e = hipSuccess;
+  const int st0 = k.kind == 1 ? 0 : k.Kr, st1 = k.kind == 1 ? k.Kr : k.Nstar;
+  if (k.kind == 1) {
+    if (k.step_ticks && (e = launch_stamp(k.step_ticks, s)) != hipSuccess) return hip_fail(c, e, "launch_stamp");
+    if ((e = launch_tr_init(a, s)) != hipSuccess) return hip_fail(c, e, "launch_tr_init");
+  }
+  for (int st = st0; st < st1; ++st) {
+    uad_status rs = enqueue_step(c, s, k.x, c->tr_t + st * M, c->tr_dt + st * M, c->tr_mask + st * M, nullptr, 0, st,
+                                 nullptr, nullptr, nullptr, k.B, k.H, k.kind == 1 && k.reconcile ? c->tr_vsum : nullptr,
+                                 k.U);
+    if (rs != UAD_OK) return rs;
+    if (k.step_ticks && (e = launch_stamp(k.step_ticks + st + 1, s)) != hipSuccess)
+      return hip_fail(c, e, "launch_stamp");
+  }
+  if (k.kind == 1 && (e = launch_tr_release(a, s)) != hipSuccess) return hip_fail(c, e, "launch_tr_release");
+  if (k.kind == 2 && k.executed && (e = launch_gac(a, s)) != hipSuccess) return hip_fail(c, e, "launch_gac");
+  return UAD_OK;
+}
+
+static uad_status enqueue_work(uad_ctx *c, hipStream_t s, const GraphKey &k) {
+  return k.kind == 0 ? enqueue_schedule(c, s, k) : enqueue_release_phase(c, s, k);
+}
+
 // Run the work described by k: replay a cached hipGraph of it when possible
 // (one graph launch for the whole schedule), else capture one; direct launches
 // while profiling or in the synthetic-velocity test mode.
@@ -653,7 +703,7 @@ static uad_status run_work(uad_ctx *c, GraphKey k) {
   k.prefix_len = c->prefix_len;
   k.prefix_batch = c->prefix_batch;
   // the measurement hook and the synthetic-velocity test mode launch directly
-  if (c->dbg || c->graph_broken || c->prof_on) return enqueue_schedule(c, c->stream, k);
+  if (c->dbg || c->graph_broken || c->prof_on) return enqueue_work(c, c->stream, k);
   ++c->graph_clock;
   uad_ctx::GraphEntry *hit = nullptr;
   for (auto &ge : c->graphs)
@@ -663,9 +713,9 @@ static uad_status run_work(uad_ctx *c, GraphKey k) {
     if (e != hipSuccess) {
       (void)hipGetLastError();
       c->graph_broken = true;
-      return enqueue_schedule(c, c->stream, k);
+      return enqueue_work(c, c->stream, k);
     }
-    uad_status rs = enqueue_schedule(c, c->cap_stream, k);
+    uad_status rs = enqueue_work(c, c->cap_stream, k);
     hipGraph_t graph = nullptr;
     e = hipStreamEndCapture(c->cap_stream, &graph);
     if (rs != UAD_OK) {
@@ -678,7 +728,7 @@ static uad_status run_work(uad_ctx *c, GraphKey k) {
     if (e != hipSuccess) {
       (void)hipGetLastError();
       c->graph_broken = true;
-      return enqueue_schedule(c, c->stream, k);
+      return enqueue_work(c, c->stream, k);
     }
     if (c->graphs.size() >= 8) {  // evict the least recently used graph
       size_t lru = 0;
@@ -703,6 +753,7 @@ uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *d
   if (st != UAD_OK) return st;
   (void)hipSetDevice(c->device);
   GraphKey k{};
+  k.kind = 0;
   k.is_schedule = false;
   k.x = x; k.t = t; k.dt = dt; k.mask = mask; k.v_out = v_out; k.n_steps = 1; k.B = batch; k.H = chunk;
   return run_work(c, k);
@@ -717,9 +768,85 @@ uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, cons
   if (n_steps < 1) return fail(c, UAD_E_INVALID, "uad_denoise_schedule: n_steps must be >= 1");
   (void)hipSetDevice(c->device);
   GraphKey k{};
+  k.kind = 0;
   k.is_schedule = true;
   k.x = x; k.t = t_sched; k.dt = dt_sched; k.mask = mask_sched; k.n_steps = n_steps; k.B = batch; k.H = chunk;
   k.released = released; k.release_step = release_step; k.step_ticks = step_ticks;
+  return run_work(c, k);
+}
+
+uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chunk, int32_t U, int32_t K,
+                               int32_t Nstar, int32_t S, int32_t mode, float *urgent_out, float *executed_out,
+                               const uint8_t *gac_mask, float *urgent_host, void *release_event,
+                               uint64_t *step_ticks) {
+  if (!c) return UAD_E_INVALID;
+  const char *fn = "uad_denoise_release";
+  if (!x || !urgent_out) return fail(c, UAD_E_INVALID, std::string(fn) + ": null x/urgent_out");
+  if (batch < 1 || chunk < 1) return fail(c, UAD_E_INVALID, std::string(fn) + ": batch and chunk must be >= 1");
+  if (batch > c->cfg.max_batch || chunk > c->cfg.max_chunk)
+    return fail(c, UAD_E_SHAPE, std::string(fn) + ": batch/chunk beyond the context maxima");
+  if (mode != UAD_RELEASE_UAER && mode != UAD_RELEASE_TR) return fail(c, UAD_E_INVALID, std::string(fn) + ": bad mode");
+  if (!(1 <= K && K < Nstar && Nstar <= kMaxTrSteps))
+    return fail(c, UAD_E_INVALID, std::string(fn) + ": need 1 <= K < N* <= 64");
+  if (!(1 <= U && U < S && S <= chunk)) return fail(c, UAD_E_INVALID, std::string(fn) + ": need 1 <= U < S <= chunk");
+  if (executed_out && mode != UAD_RELEASE_TR)
+    return fail(c, UAD_E_INVALID, std::string(fn) + ": Ghost Action Correction needs Trajectory Reconciliation");
+  if (!c->dbg) {
+    if (!c->weights_loaded) return fail(c, UAD_E_STATE, std::string(fn) + ": weights not loaded");
+    if (!c->prefix_set) return fail(c, UAD_E_STATE, std::string(fn) + ": prefix K/V not set");
+    if (batch > c->prefix_batch) return fail(c, UAD_E_STATE, std::string(fn) + ": prefix set for fewer environments");
+  }
+  (void)hipSetDevice(c->device);
+  const int reconcile = mode == UAD_RELEASE_TR ? 1 : 0;
+  const size_t M = (size_t)batch * chunk;
+  // step tables: steps < K from the budgets (K urgent, N* tail); later steps from
+  // the uniform N* schedule with TR, else from the budgets (urgent frozen)
+  const int key[6] = {batch, chunk, U, K, Nstar, reconcile};
+  if (!std::equal(key, key + 6, c->tr_key)) {
+    std::vector<int32_t> bud(M, Nstar), uni(M, Nstar);
+    for (int b = 0; b < batch; ++b)
+      for (int i = 0; i < U; ++i) bud[(size_t)b * chunk + i] = K;
+    std::vector<float> t1(Nstar * M), d1(Nstar * M), t2(Nstar * M), d2(Nstar * M);
+    std::vector<uint8_t> m1(Nstar * M), m2(Nstar * M);
+    int32_t n1 = 0, n2 = 0;
+    std::string err;
+    if (!build_schedule_host(bud.data(), batch, chunk, Nstar, &n1, t1.data(), d1.data(), m1.data(), &err) ||
+        !build_schedule_host(uni.data(), batch, chunk, Nstar, &n2, t2.data(), d2.data(), m2.data(), &err))
+      return fail(c, UAD_E_INVALID, std::string(fn) + ": " + err);
+    if (reconcile) {
+      std::copy(t2.begin() + K * M, t2.end(), t1.begin() + K * M);
+      std::copy(d2.begin() + K * M, d2.end(), d1.begin() + K * M);
+      std::copy(m2.begin() + K * M, m2.end(), m1.begin() + K * M);
+    }
+    // the tables may be in use by queued work of the previous configuration
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e == hipSuccess) e = hipMemcpy(c->tr_t, t1.data(), Nstar * M * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(c->tr_dt, d1.data(), Nstar * M * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(c->tr_mask, m1.data(), Nstar * M, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(c, e, "uad_denoise_release: step tables");
+    std::copy(key, key + 6, c->tr_key);
+  }
+  GraphKey k{};
+  k.kind = 1;
+  k.x = x; k.B = batch; k.H = chunk; k.n_steps = Nstar; k.step_ticks = step_ticks;
+  k.U = U; k.Kr = K; k.Nstar = Nstar; k.S = S; k.reconcile = reconcile;
+  k.urgent = urgent_out; k.executed = executed_out; k.gac_mask = gac_mask;
+  uad_status rs = run_work(c, k);
+  if (rs != UAD_OK) return rs;
+  // release: the urgent actions are final here; copy them to the host on the
+  // release stream while the tail continues on the context stream
+  hipError_t e = hipEventRecord(c->ev_rel, c->stream);
+  if (e == hipSuccess && urgent_host) {
+    e = hipStreamWaitEvent(c->rel_stream, c->ev_rel, 0);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(urgent_host, urgent_out, (size_t)batch * U * c->Da * sizeof(float), hipMemcpyDeviceToHost,
+                         c->rel_stream);
+    if (e == hipSuccess && release_event) e = hipEventRecord((hipEvent_t)release_event, c->rel_stream);
+  } else if (e == hipSuccess && release_event) {
+    e = hipEventRecord((hipEvent_t)release_event, c->stream);
+  }
+  if (e != hipSuccess) return hip_fail(c, e, "uad_denoise_release: release");
+  k.kind = 2;
   return run_work(c, k);
 }
 

@@ -48,6 +48,7 @@ typedef _Float16 op_t;
 // W[16*nt + (l & 15)][32*kb + 8*(l >> 4) + e], e = 0..7.  Blocks are stored
 // n-tile major, so one 16-column tile's whole K stream is contiguous and each
 // lane's operand is one aligned 16-byte load.
+constexpr int kMaxTrSteps = 64;  // longest canonical schedule N* of the release path
 constexpr int kTileN = 16;
 constexpr int kTileK = 32;
 constexpr int kBlockElems = kTileN * kTileK;  // 512 fp16 = 1 KiB
@@ -149,6 +150,23 @@ struct FinalArgs {
   int32_t *release_step;// [M] or null
   int debug_field;
   float dbg_alpha, dbg_beta;
+  // Trajectory Reconciliation: vsum[m] += v for tokens (m % chunk) < vsum_tokens
+  float *vsum;          // [M][Da] or null
+  int vsum_tokens, chunk;
+};
+
+// Urgency-aware release with Trajectory Reconciliation and Ghost Action
+// Correction over a batch of chunks (x [B][H][Da]).
+struct TrArgs {
+  float *x;              // live states
+  float *x0;             // initial noise (copy)
+  float *vsum;           // sum of the urgent tokens' velocities over steps < K
+  float *urgent;         // [B][U][Da] released urgent actions x_K
+  float *executed;       // [B][S][Da] urgent actions then GAC-corrected tail, or null
+  const uint8_t *gac_mask;  // [Da] 1 = additive dimension corrected, or null (all)
+  int B, H, Da, U, S;
+  float dt_star;         // -(1/N*), the canonical step
+  int reconcile;         // 1: TR (ghosts continue), 0: plain early release (urgent frozen)
 };
 
 // ---------------------------------------------------------------------------
@@ -169,6 +187,9 @@ hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, con
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
+hipError_t launch_tr_init(const TrArgs &a, hipStream_t s);     // x0 <- x, vsum <- 0
+hipError_t launch_tr_release(const TrArgs &a, hipStream_t s);  // urgent <- x_K; TR: x_K <- x0 + dt* vsum
+hipError_t launch_gac(const TrArgs &a, hipStream_t s);         // E and the corrected executed actions
 
 // Host-side helpers (schedule.cpp)
 bool build_schedule_host(const int32_t *budgets, int batch, int chunk, int max_steps, int32_t *n_steps,
@@ -181,6 +202,7 @@ bool build_schedule_host(const int32_t *budgets, int batch, int chunk, int max_s
 // ---------------------------------------------------------------------------
 // Everything a captured step/schedule graph depends on.
 struct GraphKey {
+  int kind;  // 0: step / schedule; 1, 2: urgency-aware release phases before / after the release
   bool is_schedule;
   float *x;
   const float *t, *dt;
@@ -189,8 +211,14 @@ struct GraphKey {
   int32_t *release_step;
   uint64_t *step_ticks;
   int n_steps, B, H, prefix_len, prefix_batch;
+  // release phases
+  int U, Kr, Nstar, S, reconcile;
+  float *urgent, *executed;
+  const uint8_t *gac_mask;
   bool operator==(const GraphKey &o) const {
-    return is_schedule == o.is_schedule && x == o.x && t == o.t && dt == o.dt && mask == o.mask &&
+    return kind == o.kind && U == o.U && Kr == o.Kr && Nstar == o.Nstar && S == o.S && reconcile == o.reconcile &&
+           urgent == o.urgent && executed == o.executed && gac_mask == o.gac_mask &&
+           is_schedule == o.is_schedule && x == o.x && t == o.t && dt == o.dt && mask == o.mask &&
            v_out == o.v_out && released == o.released && release_step == o.release_step &&
            step_ticks == o.step_ticks && n_steps == o.n_steps && B == o.B && H == o.H &&
            prefix_len == o.prefix_len && prefix_batch == o.prefix_batch;
@@ -237,6 +265,14 @@ struct uad_ctx {
   size_t attn_part_elems = 0;
   float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]
   void *abuf = nullptr;
+
+  // urgency-aware release with Trajectory Reconciliation
+  float *tr_x0 = nullptr, *tr_vsum = nullptr;  // [m_alloc][Da]
+  float *tr_t = nullptr, *tr_dt = nullptr;     // [kMaxSteps][m_alloc] step tables of the last configuration
+  uint8_t *tr_mask = nullptr;
+  int tr_key[6] = {0, 0, 0, 0, 0, -1};         // B, H, U, K, N*, reconcile of the tables
+  hipStream_t rel_stream = nullptr;            // release copies
+  hipEvent_t ev_rel = nullptr;
 
   // captured step / schedule graphs (small LRU cache)
   struct GraphEntry {

@@ -42,6 +42,20 @@ class ActionExpert:
     def schedule(self, x, t_sched, dt_sched, mask_sched, released=None, release_step=None, step_ticks=None):
         B.uad_denoise_schedule(self.ctx, x, t_sched, dt_sched, mask_sched, released, release_step, step_ticks)
 
+    def release(self, x, U: int, K: int, Nstar: int, S: int, reconcile: bool = True, urgent=None,
+                executed=None, gac_mask=None, urgent_host=None, release_event=None, step_ticks=None):
+        """Urgency-aware release (UAER, or TR + ghosts, GAC when ``executed`` is given).
+
+        Allocates ``urgent`` [B][U][Da] on the device when not given and returns it.
+        """
+        B_, H_, Da = x.shape
+        if urgent is None:
+            urgent = torch.empty((B_, U, Da), dtype=torch.float32, device=x.device)
+        mode = B.UAD_RELEASE_TR if reconcile else B.UAD_RELEASE_UAER
+        B.uad_denoise_release(self.ctx, x, U, K, Nstar, S, mode, urgent, executed, gac_mask, urgent_host,
+                              release_event, step_ticks)
+        return urgent
+
     def debug_velocity_field(self, enable: bool, alpha: float = 0.0, beta: float = 0.0) -> None:
         B.uad_debug_velocity_field(self.ctx, enable, alpha, beta)
 
