@@ -82,15 +82,28 @@ def step_flops(wl):
     return 2 * M * W.weight_param_count(s) + att
 
 
-def cpu_baseline(wl, weights, prefix, noise, budgets, seconds):
-    """Time the oracle (as it stands) on this host for a bounded sample of joint steps."""
+def cpu_baseline(wl, weights, prefix, noise, budgets, seconds, limit_threads=None):
+    """Time the oracle (as it stands) on this host for a bounded sample of joint steps
+    (BLAS threads capped at ``limit_threads`` when given)."""
+    import contextlib
     import numpy as np
     import oracle as O
+    ctx = contextlib.nullcontext()
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        if limit_threads is not None:
+            ctx = threadpool_limits(limits=limit_threads)
     except Exception:
-        threads = os.cpu_count() or 1
+        threadpool_info = None
+    with ctx:
+        if threadpool_info is not None:
+            threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+        else:
+            threads = os.cpu_count() or 1
+        return _cpu_baseline_run(wl, weights, prefix, noise, budgets, seconds, threads, O)
+
+
+def _cpu_baseline_run(wl, weights, prefix, noise, budgets, seconds, threads, O):
     m = O.build_model(wl.shape, weights, [p[0] for p in prefix], [p[1] for p in prefix])
     n, t, dt, mask = O.build_schedule(budgets)
     x = noise.copy()
@@ -176,6 +189,26 @@ def main():
     ms_step = 1e3 * el / steps
     log(f"[bench] timed {steps} steps: {ms_step:.4f} ms/step, {sps:.1f} steps/s")
 
+    # Per-schedule device time (ticks at schedule start / end), median and a 95%
+    # bootstrap interval over the R schedules (8000 resamples).
+    hz = ex.tick_rate_hz()
+    ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
+    per_sched = []
+    for _ in range(max(20, n_timed)):
+        x.copy_(x0)
+        ex.schedule(x, tg, dtg, mg, None, None, ticks)
+        torch.cuda.synchronize()
+        tk = ticks.numpy().astype(np.int64)
+        per_sched.append((tk[-1] - tk[0]) / hz * 1e3)
+    per_sched = np.array(per_sched)
+    rng = np.random.default_rng(0)
+    boot = np.median(rng.choice(per_sched, size=(8000, per_sched.size), replace=True), axis=1)
+    sched_stats = {"schedules": int(per_sched.size), "steps_per_schedule": int(n),
+                   "median_ms": round(float(np.median(per_sched)), 4),
+                   "ci95_ms": [round(float(np.percentile(boot, 2.5)), 4), round(float(np.percentile(boot, 97.5)), 4)],
+                   "clock": "device wall-clock ticks around each schedule (stamp kernels)"}
+    log(f"[bench] schedule median {sched_stats['median_ms']} ms, 95% CI {sched_stats['ci95_ms']}")
+
     # Per-kernel durations: the same schedules again, launched directly with a
     # start/stop HIP event pair taken from each kernel's dispatch packet, on the
     # stream the kernels run on (the library's measurement hook).
@@ -224,7 +257,7 @@ def main():
         "config": {"workload": wl.name, "batch": B, "chunk": H, "prefix": P, "layers": s.n_layers,
                    "width": s.d_model, "heads": f"{s.n_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.d_ff,
                    "action_dim": s.action_dim, "schedule": f"{wl.budget_kind} {n} steps"},
-        "roofline": roof, "step_roofline": step_roof, "kernels": per_kernel,
+        "roofline": roof, "step_roofline": step_roof, "schedule_time": sched_stats, "kernels": per_kernel,
     }
 
     if not a.no_aal and B == 1:
@@ -233,42 +266,88 @@ def main():
     if not a.no_cpu_baseline:
         log("[bench] timing the oracle on the host cores")
         out["cpu_baseline"] = cpu_baseline(wl, weights, prefix, noise, budgets, a.cpu_seconds)
+        one = cpu_baseline(wl, weights, prefix, noise, budgets, a.cpu_seconds / 2, limit_threads=1)
+        out["cpu_baseline_1thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
     print(json.dumps(out), flush=True)
     ex.close()
 
 
 def availability(ex, wl, noise, U, np, torch, reps=20):
-    """Release times of the S executed actions and AAL (App. B / App. C.3) for the
-    vanilla uniform schedule and the UAD 4/7/10 schedule on this model."""
-    import uad_workloads as W
-    hz = ex.tick_rate_hz()
-    S = wl.executed
-    res = {}
-    sched = {"vanilla_uniform_10": np.full((1, wl.chunk), 10, np.int32),
-             "uad_4_7_10": W.make_budgets(W.get_workload("pi0_b1_uad"))}
-    for name, bud in sched.items():
-        n, tg, dtg, mg = ex.schedule_tables(bud)
-        x0 = torch.from_numpy(noise).cuda()
-        x = torch.empty_like(x0)
-        ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
-        rst = torch.zeros((1, wl.chunk), dtype=torch.int32, device="cuda")
-        step_ms = []
+    """Action-availability latency on this model (App. B timing model, App. C.3
+    measurement, T_VLM = 0 since the prefix is given).
+
+    Release time of each of the S executed actions, measured on the host from the
+    call to the moment the action is host-visible: vanilla uniform N* (all S
+    actions when the chunk is done) and UAD with Trajectory Reconciliation and
+    Ghost Action Correction at K = 1 (urgent actions when the release event fires,
+    tail actions when the chunk is done), at the paper's (U, N*) settings.
+    AAL replays the controller for T_act = 50 and 12.5 ms.  The U sweep gives the
+    average blocking time of the tail actions (App. C, u_sweep) at N* = 7.
+    """
+    S, H, Da = wl.executed, wl.chunk, wl.shape.action_dim
+    x0 = torch.from_numpy(noise).cuda()
+    x = torch.empty_like(x0)
+
+    def vanilla(Ns):
+        n, tg, dtg, mg = ex.schedule_tables(np.full((1, H), Ns, np.int32))
+        ts = []
         for r in range(reps + 2):
             x.copy_(x0)
-            ex.schedule(x, tg, dtg, mg, None, rst, ticks)
             torch.cuda.synchronize()
-            tk = ticks.numpy().astype(np.int64)
+            t0 = time.perf_counter()
+            ex.schedule(x, tg, dtg, mg)
+            torch.cuda.synchronize()
             if r >= 2:
-                step_ms.append((tk[1:] - tk[0]) / hz * 1e3)
-        step_ms = np.median(np.stack(step_ms), axis=0)  # time at the end of each step
-        rs = rst.cpu().numpy()[0, :S]
-        rel = [float(step_ms[k]) for k in rs]
+                ts.append((time.perf_counter() - t0) * 1e3)
+        t_end = float(np.median(ts))
+        return [t_end] * S
+
+    def uad(Ns, U_, K=1):
+        urgent = torch.empty((1, U_, Da), device="cuda")
+        executed = torch.empty((1, S, Da), device="cuda")
+        host = torch.empty((1, U_, Da)).pin_memory()
+        ev = torch.cuda.Event()
+        tr, te = [], []
+        for r in range(reps + 2):
+            x.copy_(x0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            ex.release(x, U_, K, Ns, S, urgent=urgent, executed=executed, urgent_host=host, release_event=ev)
+            ev.synchronize()
+            t1 = time.perf_counter()
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            if r >= 2:
+                tr.append((t1 - t0) * 1e3)
+                te.append((t2 - t0) * 1e3)
+        r_u, r_t = float(np.median(tr)), float(np.median(te))
+        return [r_u] * U_ + [r_t] * (S - U_)
+
+    def summarise(rel):
         ent = {"release_ms_executed": [round(v, 4) for v in rel], "ttfr_ms": round(min(rel), 4)}
         for tact in (50.0, 12.5):
             ent[f"aal_ms_tact_{tact:g}"] = round(U.uad_aal(rel, tact), 5)
-        res[name] = ent
-    v, u = res["vanilla_uniform_10"], res["uad_4_7_10"]
-    res["aal_speedup_tact_12.5"] = round(v["aal_ms_tact_12.5"] / u["aal_ms_tact_12.5"], 3)
+        return ent
+
+    res = {"clock": "host wall-clock from the call to host visibility (median of %d)" % reps}
+    for Ns, U_ in ((7, 5), (3, 3), (2, 2), (10, 5)):
+        v = summarise(vanilla(Ns))
+        u = summarise(uad(Ns, U_))
+        res[f"N*={Ns}"] = {"vanilla": v, f"uad_tr_gac_K1_U{U_}": u,
+                           "aal_speedup_tact_12.5": round(v["aal_ms_tact_12.5"] / u["aal_ms_tact_12.5"], 3),
+                           "aal_speedup_tact_50": round(v["aal_ms_tact_50"] / u["aal_ms_tact_50"], 3)}
+    sweep = {}
+    for U_ in range(1, S):
+        rel = uad(7, U_)
+        for tact in (12.5,):
+            clock, waits = 0.0, []
+            for j, r in enumerate(rel):
+                w = max(0.0, r - clock)
+                clock = max(clock, r) + tact
+                if j >= U_:
+                    waits.append(w)
+        sweep[str(U_)] = round(float(np.mean(waits)), 5)
+    res["u_sweep_tail_blocking_ms_Nstar7_tact12.5"] = sweep
     return res
 
 
