@@ -44,6 +44,13 @@ Readings where the paper is silent (each is also listed in the design notes):
    x + 0*v, so it stays bit-identical whatever v holds.
 8. Ghost tokens after reconciliation run at t = (N* - k)/N*, dt = -(1/N*),
    and the reconciliation sum accumulates the cached velocities in step order.
+9. Adaptive-norm conditioning (the pi0.5-style expert, App. C.1; the paper
+   names the mechanism but gives no formula): c = SiLU(W_t2 SiLU(W_t1 e(t) +
+   b_t1) + b_t2) per token; the action token is h_0 = W_in x + b_in; every
+   norm site s (attention and MLP of each layer) takes (alpha, beta, gamma) =
+   W_s c + b_s and computes n = RMS(h) * (1 + alpha) + beta (no separate
+   gain), the branch output enters the residual as h += gamma * branch; the
+   final norm takes (alpha_f, beta_f) = W_f c + b_f.
 
 Precision: fp32 throughout (the numpy matmuls are BLAS sgemm), or float64 when
 a model is built with ``dtype=np.float64``.  The time-embedding arguments are
@@ -57,7 +64,7 @@ from typing import Callable, Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = [
-    "Model", "build_model", "rms_norm", "silu", "gelu_tanh", "time_embedding",
+    "Model", "build_model", "rms_norm", "ada_rms_norm", "silu", "gelu_tanh", "time_embedding",
     "time_frequencies", "attention", "action_expert", "velocity", "euler_update",
     "build_schedule", "denoise_step", "denoise_schedule", "vanilla_denoise",
     "release_steps", "uad_tr_gac", "gac_correct", "aal_controller",
@@ -82,6 +89,7 @@ class Model:
     prefix_k: List[np.ndarray]   # per env: [L][P][Hkv][hd]
     prefix_v: List[np.ndarray]
     dtype: type = np.float32
+    conditioning: str = "input"  # "input" (reading 3) or "adarms" (reading 9)
 
 
 def build_model(shape, weights: Dict[str, np.ndarray], prefix_k: Sequence[np.ndarray],
@@ -90,7 +98,8 @@ def build_model(shape, weights: Dict[str, np.ndarray], prefix_k: Sequence[np.nda
     return Model(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads,
                  shape.head_dim, shape.d_ff, shape.action_dim, shape.rms_eps,
                  {k: np.asarray(v, dt) for k, v in weights.items()},
-                 [np.asarray(k, dt) for k in prefix_k], [np.asarray(v, dt) for v in prefix_v], dt)
+                 [np.asarray(k, dt) for k in prefix_k], [np.asarray(v, dt) for v in prefix_v], dt,
+                 getattr(shape, "conditioning", "input"))
 
 
 # ----------------------------------------------------------------------------
@@ -100,6 +109,12 @@ def rms_norm(h: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:
     """RMSNorm over the last axis: h / sqrt(mean(h^2) + eps) * gain."""
     ms = np.mean(h * h, axis=-1, keepdims=True)
     return h / np.sqrt(ms + h.dtype.type(eps)) * gain
+
+
+def ada_rms_norm(h: np.ndarray, scale: np.ndarray, shift: np.ndarray, eps: float) -> np.ndarray:
+    """Adaptive RMSNorm (reading 9): h / sqrt(mean(h^2) + eps) * (1 + scale) + shift."""
+    r = h / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + h.dtype.type(eps))
+    return r * (h.dtype.type(1) + scale) + shift
 
 
 def silu(z: np.ndarray) -> np.ndarray:
@@ -157,6 +172,8 @@ def action_expert(m: Model, env: int, x: np.ndarray, t: np.ndarray) -> np.ndarra
 
     x [H, Da] noisy actions, t [H] per-token flow time -> velocity [H, Da].
     """
+    if m.conditioning == "adarms":
+        return _action_expert_adarms(m, env, x, t)
     W, dt = m.weights, m.dtype
     x = np.asarray(x, dt)
     t = np.asarray(t, dt)
@@ -181,6 +198,37 @@ def action_expert(m: Model, env: int, x: np.ndarray, t: np.ndarray) -> np.ndarra
         g = gelu_tanh(n2 @ W[p + "w_gate"].T) * (n2 @ W[p + "w_up"].T)
         h = h + g @ W[p + "w_down"].T
     nf = rms_norm(h, W["final_norm"], m.rms_eps)
+    return nf @ W["action_out.w"].T + W["action_out.b"]
+
+
+def _action_expert_adarms(m: Model, env: int, x: np.ndarray, t: np.ndarray) -> np.ndarray:
+    """The expert with adaptive-norm time conditioning (App. C.1, reading 9)."""
+    W, dt = m.weights, m.dtype
+    x = np.asarray(x, dt)
+    t = np.asarray(t, dt)
+    H, d = x.shape[0], m.d_model
+    e = time_embedding(t, d)
+    c = silu(silu(e @ W["time_mlp_in.w"].T + W["time_mlp_in.b"]) @ W["time_mlp_out.w"].T + W["time_mlp_out.b"])
+    h = x @ W["action_in.w"].T + W["action_in.b"]
+    for l in range(m.n_layers):
+        p = f"layers.{l}."
+        ma = c @ W[p + "attn_mod.w"].T + W[p + "attn_mod.b"]
+        al, be, ga = ma[:, :d], ma[:, d:2 * d], ma[:, 2 * d:]
+        n = ada_rms_norm(h, al, be, m.rms_eps)
+        q = (n @ W[p + "wq"].T).reshape(H, m.n_heads, m.head_dim)
+        k = (n @ W[p + "wk"].T).reshape(H, m.n_kv_heads, m.head_dim)
+        v = (n @ W[p + "wv"].T).reshape(H, m.n_kv_heads, m.head_dim)
+        k_all = np.concatenate([m.prefix_k[env][l], k], axis=0)
+        v_all = np.concatenate([m.prefix_v[env][l], v], axis=0)
+        o = attention(q, k_all, v_all).reshape(H, m.n_heads * m.head_dim)
+        h = h + ga * (o @ W[p + "wo"].T)
+        mm = c @ W[p + "mlp_mod.w"].T + W[p + "mlp_mod.b"]
+        al, be, ga = mm[:, :d], mm[:, d:2 * d], mm[:, 2 * d:]
+        n2 = ada_rms_norm(h, al, be, m.rms_eps)
+        g = gelu_tanh(n2 @ W[p + "w_gate"].T) * (n2 @ W[p + "w_up"].T)
+        h = h + ga * (g @ W[p + "w_down"].T)
+    mf = c @ W["final_mod.w"].T + W["final_mod.b"]
+    nf = ada_rms_norm(h, mf[:, :d], mf[:, d:], m.rms_eps)
     return nf @ W["action_out.w"].T + W["action_out.b"]
 
 

@@ -79,3 +79,70 @@ def forward_env(W, shape, pk, pv, x, t):
         nf = _rms(hs[i], W["final_norm"], eps)
         out.append([v + b for v, b in zip(_matvec(W["action_out.w"], nf), W["action_out.b"])])
     return out
+
+
+def _adarms(h, scale, shift, eps):
+    # h / rms(h) * (1 + scale_c) + shift_c, every term spelled out
+    ms = sum(v * v for v in h) / len(h)
+    r = 1.0 / math.sqrt(ms + eps)
+    return [h[c] * r * (1.0 + scale[c]) + shift[c] for c in range(len(h))]
+
+
+def forward_env_adarms(W, shape, pk, pv, x, t):
+    """The adaptive-norm-conditioned expert, token by token (same arguments as forward_env)."""
+    L, d, Hq, Hkv, hd = shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim
+    eps = shape.rms_eps
+    H = len(x)
+    cs, hs = [], []
+    for i in range(H):
+        e = _temb(t[i], d)
+        z = [_silu(v + b) for v, b in zip(_matvec(W["time_mlp_in.w"], e), W["time_mlp_in.b"])]
+        cs.append([_silu(v + b) for v, b in zip(_matvec(W["time_mlp_out.w"], z), W["time_mlp_out.b"])])
+        hs.append([v + b for v, b in zip(_matvec(W["action_in.w"], x[i]), W["action_in.b"])])
+
+    def mod(name, i):
+        return [v + b for v, b in zip(_matvec(W[name + ".w"], cs[i]), W[name + ".b"])]
+
+    for l in range(L):
+        p = f"layers.{l}."
+        ns = []
+        gates = []
+        for i in range(H):
+            m = mod(p + "attn_mod", i)
+            ns.append(_adarms(hs[i], m[:d], m[d:2 * d], eps))
+            gates.append(m[2 * d:])
+        qs = [_matvec(W[p + "wq"], n) for n in ns]
+        ks = [_matvec(W[p + "wk"], n) for n in ns]
+        vs = [_matvec(W[p + "wv"], n) for n in ns]
+        P = len(pk[l])
+        new_h = []
+        for i in range(H):
+            o = []
+            for j in range(Hq):
+                g = (j * Hkv) // Hq
+                keys = [pk[l][s][g] for s in range(P)] + [ks[s][g * hd:(g + 1) * hd] for s in range(H)]
+                vals = [pv[l][s][g] for s in range(P)] + [vs[s][g * hd:(g + 1) * hd] for s in range(H)]
+                qj = qs[i][j * hd:(j + 1) * hd]
+                sc = [sum(qj[c] * kk[c] for c in range(hd)) / math.sqrt(hd) for kk in keys]
+                mx = max(sc)
+                ex = [math.exp(s - mx) for s in sc]
+                den = sum(ex)
+                for c in range(hd):
+                    o.append(sum(ex[s] * vals[s][c] for s in range(len(keys))) / den)
+            ao = _matvec(W[p + "wo"], o)
+            new_h.append([hs[i][c] + gates[i][c] * ao[c] for c in range(d)])
+        hs = new_h
+        for i in range(H):
+            m = mod(p + "mlp_mod", i)
+            n2 = _adarms(hs[i], m[:d], m[d:2 * d], eps)
+            gate = _matvec(W[p + "w_gate"], n2)
+            up = _matvec(W[p + "w_up"], n2)
+            gg = [_gelu(gate[c]) * up[c] for c in range(len(gate))]
+            dn = _matvec(W[p + "w_down"], gg)
+            hs[i] = [hs[i][c] + m[2 * d + c] * dn[c] for c in range(d)]
+    out = []
+    for i in range(H):
+        m = mod("final_mod", i)
+        nf = _adarms(hs[i], m[:d], m[d:], eps)
+        out.append([v + b for v, b in zip(_matvec(W["action_out.w"], nf), W["action_out.b"])])
+    return out

@@ -332,3 +332,72 @@ def test_aal_controller_reproduces_latency_model():
         assert abs(O.aal_controller(rel, T_act) - O.latency_uaer(T_vlm, T_D, Nstar, K, U, T_act, S)) < 1e-9
         van = [T_vlm + Nstar * T_D] * S
         assert abs(O.aal_controller(van, T_act) - O.latency_vanilla(T_vlm, T_D, Nstar, S)) < 1e-9
+
+
+# ----------------------------------------------------------------------------
+# Adaptive-norm time conditioning (App. C.1, reading 9)
+# ----------------------------------------------------------------------------
+TINY_ADA = W.ModelShape(n_layers=2, d_model=8, n_heads=2, n_kv_heads=1, head_dim=4, d_ff=12, action_dim=3,
+                        conditioning="adarms")
+
+
+def test_adarms_forward_matches_scalar_bruteforce():
+    for shape, seed in ((TINY_ADA, 21), (W.ModelShape(1, 12, 3, 3, 2, 5, 2, conditioning="adarms"), 22)):
+        m, weights, pk, pv = tiny_model(shape, P=3, seed=seed)
+        x = np.random.default_rng(seed).standard_normal((3, shape.action_dim))
+        t = np.array([1.0, 0.4, 0.0])
+        ref = bruteforce.forward_env_adarms({k: v.tolist() for k, v in weights.items()}, shape,
+                                            pk[0].tolist(), pv[0].tolist(), x.tolist(), t.tolist())
+        np.testing.assert_allclose(O.action_expert(m, 0, x, t), np.array(ref), rtol=0, atol=1e-11)
+
+
+def test_ada_rms_norm_special_cases():
+    rng = np.random.default_rng(3)
+    h = rng.standard_normal((4, 8))
+    z = np.zeros_like(h)
+    # no modulation = RMSNorm with unit gain; scale s = RMSNorm with gain 1 + s (per token)
+    np.testing.assert_allclose(O.ada_rms_norm(h, z, z, 1e-6), O.rms_norm(h, np.ones(8), 1e-6), atol=1e-15)
+    s = rng.standard_normal(8)
+    np.testing.assert_allclose(O.ada_rms_norm(h, np.broadcast_to(s, h.shape), z, 1e-6),
+                               O.rms_norm(h, 1 + s, 1e-6), atol=1e-14)
+    # constant vector c*1 normalises to sign(c) (up to eps), then (1 + a) * sign(c) + b
+    c = np.full((1, 8), -2.5)
+    a, b = rng.standard_normal((1, 8)), rng.standard_normal((1, 8))
+    np.testing.assert_allclose(O.ada_rms_norm(c, a, b, 0.0), -(1 + a) + b, atol=1e-14)
+    # torch's functional rms_norm as a library reference for the normalisation
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(h), (8,), eps=1e-6).numpy() * (1 + a) + b
+    np.testing.assert_allclose(O.ada_rms_norm(h, np.broadcast_to(a, h.shape), np.broadcast_to(b, h.shape), 1e-6),
+                               ref, atol=1e-14)
+
+
+def test_adarms_time_enters_only_through_modulation():
+    """With every modulation matrix zero, v no longer depends on t; with them, it does."""
+    m, *_ = tiny_model(TINY_ADA, seed=23)
+    x = np.random.default_rng(4).standard_normal((2, 3))
+    t1, t2 = np.array([0.9, 0.1]), np.array([0.3, 0.6])
+    assert not np.allclose(O.action_expert(m, 0, x, t1), O.action_expert(m, 0, x, t2))
+    for k in list(m.weights):
+        if k.endswith("_mod.w"):
+            m.weights[k] = np.zeros_like(m.weights[k])
+    np.testing.assert_array_equal(O.action_expert(m, 0, x, t1), O.action_expert(m, 0, x, t2))
+
+
+def test_adarms_zero_gates_closed_form():
+    """gamma = 0 on every branch: the layers do nothing and
+    v = (RMS(h_0) (1 + a_f) + b_f) W_out^T + b_out with h_0 = W_in x + b_in."""
+    m, *_ = tiny_model(TINY_ADA, seed=24)
+    d = TINY_ADA.d_model
+    for l in range(TINY_ADA.n_layers):
+        for s in ("attn_mod", "mlp_mod"):
+            m.weights[f"layers.{l}.{s}.w"][2 * d:] = 0
+            m.weights[f"layers.{l}.{s}.b"][2 * d:] = 0
+    x = np.random.default_rng(5).standard_normal((2, 3))
+    t = np.array([0.8, 0.2])
+    Wt = m.weights
+    e = O.time_embedding(t, d)
+    c = O.silu(O.silu(e @ Wt["time_mlp_in.w"].T + Wt["time_mlp_in.b"]) @ Wt["time_mlp_out.w"].T + Wt["time_mlp_out.b"])
+    h0 = x @ Wt["action_in.w"].T + Wt["action_in.b"]
+    mf = c @ Wt["final_mod.w"].T + Wt["final_mod.b"]
+    r = h0 / np.sqrt((h0 ** 2).mean(-1, keepdims=True) + 1e-6)
+    ref = (r * (1 + mf[:, :d]) + mf[:, d:]) @ Wt["action_out.w"].T + Wt["action_out.b"]
+    np.testing.assert_allclose(O.action_expert(m, 0, x, t), ref, atol=1e-12)

@@ -41,6 +41,10 @@ class ModelShape:
     d_ff: int
     action_dim: int
     rms_eps: float = 1e-6
+    # "input": time embedding concatenated to the action token before the time
+    # MLP; "adarms": time MLP output modulates every RMSNorm (scale, shift) and
+    # gates every residual branch (App. C.1, the pi0.5-style variant)
+    conditioning: str = "input"
 
 
 @dataclasses.dataclass(frozen=True)
@@ -79,7 +83,16 @@ WORKLOADS: Dict[str, Workload] = {
                           "linear", (3, 12), bf16=True),
 }
 
+# Adaptive-norm time conditioning (the pi0.5-style expert of App. C.1): the
+# tiny and pi0-scale models with modulated norms instead of input conditioning.
+WORKLOADS["tiny_adarms"] = Workload("tiny_adarms", ModelShape(2, 256, 4, 4, 64, 1024, 7, conditioning="adarms"),
+                                    1, 16, 64, "uniform", (10,), bf16=False)
+WORKLOADS["pi05_b1_adarms"] = Workload("pi05_b1_adarms",
+                                       ModelShape(18, 1024, 8, 1, 256, 4096, 32, conditioning="adarms"),
+                                       1, 50, 816, "uniform", (10,), bf16=True)
+
 WORKLOAD_ORDER = ["tiny", "pi0_b1", "pi0_b1_uad", "pi0_fleet_b64", "large_b16"]
+ADARMS_WORKLOADS = ["tiny_adarms", "pi05_b1_adarms"]
 
 
 def get_workload(name: str, **overrides) -> Workload:
@@ -94,23 +107,29 @@ def get_workload(name: str, **overrides) -> Workload:
 def weight_specs(s: ModelShape) -> List[Tuple[str, Tuple[int, ...], str]]:
     """(name, shape, init) for every named weight; init in {"w", "gain", "bias"}."""
     d, hq, hkv, hd, f, da = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim, s.d_ff, s.action_dim
+    ada = s.conditioning == "adarms"
     out = [
         ("action_in.w", (d, da), "w"), ("action_in.b", (d,), "bias"),
-        ("time_mlp_in.w", (d, 2 * d), "w"), ("time_mlp_in.b", (d,), "bias"),
+        ("time_mlp_in.w", (d, d if ada else 2 * d), "w"), ("time_mlp_in.b", (d,), "bias"),
         ("time_mlp_out.w", (d, d), "w"), ("time_mlp_out.b", (d,), "bias"),
     ]
     for l in range(s.n_layers):
         p = f"layers.{l}."
+        out += [(p + "attn_mod.w", (3 * d, d), "w"), (p + "attn_mod.b", (3 * d,), "bias")] if ada else \
+               [(p + "attn_norm", (d,), "gain")]
         out += [
-            (p + "attn_norm", (d,), "gain"),
             (p + "wq", (hq * hd, d), "w"), (p + "wk", (hkv * hd, d), "w"),
             (p + "wv", (hkv * hd, d), "w"), (p + "wo", (d, hq * hd), "w"),
-            (p + "mlp_norm", (d,), "gain"),
+        ]
+        out += [(p + "mlp_mod.w", (3 * d, d), "w"), (p + "mlp_mod.b", (3 * d,), "bias")] if ada else \
+               [(p + "mlp_norm", (d,), "gain")]
+        out += [
             (p + "w_gate", (f, d), "w"), (p + "w_up", (f, d), "w"),
             (p + "w_down", (d, f), "w"),
         ]
-    out += [("final_norm", (d,), "gain"), ("action_out.w", (da, d), "w"),
-            ("action_out.b", (da,), "bias")]
+    out += [("final_mod.w", (2 * d, d), "w"), ("final_mod.b", (2 * d,), "bias")] if ada else \
+           [("final_norm", (d,), "gain")]
+    out += [("action_out.w", (da, d), "w"), ("action_out.b", (da,), "bias")]
     return out
 
 
