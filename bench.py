@@ -41,14 +41,19 @@ def kernel_bytes(wl, M):
     d, F, qd, kvd = s.d_model, s.d_ff, s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
     nqkv = qd + 2 * kvd
     keys = wl.prefix + wl.chunk
-    return {
+    ada = getattr(s, "conditioning", "input") == "adarms"
+    out = {} if not ada else {
+        # every norm site's (scale, shift, gate) per token, fp32 out
+        "gemm_mod": gemm_bytes(M, (6 * s.n_layers + 2) * d, d, M * (6 * s.n_layers + 2) * d * 4),
+    }
+    return out | {
         "gemm_qkv": gemm_bytes(M, nqkv, d, M * nqkv * 2),
         "attention": wl.batch * s.n_kv_heads * keys * s.head_dim * 2 * 2 + M * qd * 2 * 2,
         "gemm_o": gemm_bytes(M, d, qd, M * d * 4 * 2),
         "gemm_gateup": gemm_bytes(M, 2 * F, d, M * F * 2),
         "gemm_down": gemm_bytes(M, d, F, M * d * 4 * 2),
-        "gemm_time_in": gemm_bytes(M, d, 2 * d, M * d * 2),
-        "gemm_time_out": gemm_bytes(M, d, d, M * d * 4),
+        "gemm_time_in": gemm_bytes(M, d, d if ada else 2 * d, M * d * 2),
+        "gemm_time_out": gemm_bytes(M, d, d, M * d * (2 if ada else 4)),
     }
 
 
@@ -56,13 +61,14 @@ def kernel_flops(wl, M):
     s = wl.shape
     d, F, qd, kvd = s.d_model, s.d_ff, s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
     keys = wl.prefix + wl.chunk
-    return {
+    ada = getattr(s, "conditioning", "input") == "adarms"
+    return ({"gemm_mod": 2 * M * d * (6 * s.n_layers + 2) * d} if ada else {}) | {
         "gemm_qkv": 2 * M * d * (qd + 2 * kvd),
         "attention": 4 * wl.batch * s.n_heads * wl.chunk * keys * s.head_dim,
         "gemm_o": 2 * M * qd * d,
         "gemm_gateup": 2 * M * d * 2 * F,
         "gemm_down": 2 * M * F * d,
-        "gemm_time_in": 2 * M * 2 * d * d,
+        "gemm_time_in": 2 * M * (1 if ada else 2) * d * d,
         "gemm_time_out": 2 * M * d * d,
     }
 

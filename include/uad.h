@@ -38,6 +38,17 @@
  *    query head j uses KV head floor(j*Hkv/Hq), scale 1/sqrt(hd)) -> output
  *    projection + residual -> RMSNorm -> GeGLU (tanh GELU) MLP + residual;
  *    final RMSNorm and action projection give the velocity.
+ *  - With UAD_FLAG_ADARMS (adaptive-norm time conditioning, the pi0.5-style
+ *    expert of App. C.1) the time embedding no longer enters the action token:
+ *    h_0 = W_in x + b_in, and c = SiLU(W_t2 SiLU(W_t1 e(t) + b_t1) + b_t2) per
+ *    token modulates every norm: for each norm site (a, b, g) = W c + b gives
+ *    n = RMSNorm_unit(h) * (1 + a) + b and the branch enters the residual as
+ *    h += g * branch; the final norm takes (a, b) only.  Weight names then are
+ *      time_mlp_in.w [d][d] (instead of [d][2d]),
+ *      layers.<l>.attn_mod.w [3d][d], layers.<l>.attn_mod.b [3d],
+ *      layers.<l>.mlp_mod.w [3d][d], layers.<l>.mlp_mod.b [3d],
+ *      final_mod.w [2d][d], final_mod.b [2d],
+ *    rows ordered (a | b | g), replacing attn_norm, mlp_norm and final_norm.
  */
 #ifndef UAD_H
 #define UAD_H
@@ -75,8 +86,11 @@ typedef struct {
   int32_t max_chunk;  /* largest chunk H of any later call */
   int32_t max_prefix; /* largest prefix length P */
   float rms_eps;      /* RMSNorm epsilon (1e-6 in the bundled workloads) */
-  int32_t flags;      /* reserved, must be 0 */
+  int32_t flags;      /* 0 or UAD_FLAG_ADARMS */
 } uad_model_config;
+
+/* uad_model_config.flags: adaptive-norm time conditioning (see the top). */
+enum { UAD_FLAG_ADARMS = 1 };
 
 typedef struct {
   const char *name;  /* one of the names listed above */

@@ -20,12 +20,13 @@ __all__ = [
     "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_denoise_release",
     "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
     "uad_profile_enable", "uad_profile_read", "UAD_DTYPE_F32", "UAD_DTYPE_BF16", "STATUS_NAMES",
-    "UAD_RELEASE_UAER", "UAD_RELEASE_TR",
+    "UAD_RELEASE_UAER", "UAD_RELEASE_TR", "UAD_FLAG_ADARMS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libuad.so")
 UAD_DTYPE_F32, UAD_DTYPE_BF16 = 0, 1
 UAD_RELEASE_UAER, UAD_RELEASE_TR = 0, 1
+UAD_FLAG_ADARMS = 1
 STATUS_NAMES = {0: "UAD_OK", 1: "UAD_E_INVALID", 2: "UAD_E_SHAPE", 3: "UAD_E_STATE", 4: "UAD_E_MISSING",
                 5: "UAD_E_HIP", 6: "UAD_E_OOM", 7: "UAD_E_UNSUPPORTED"}
 EXPORTED_SYMBOLS = [
@@ -123,9 +124,10 @@ def uad_create(shape, max_batch: int, max_chunk: int, max_prefix: int, device: i
                stream: Optional[torch.cuda.Stream] = None) -> int:
     """Create a context for a model shape (fields as ``uad_workloads.ModelShape``); returns a handle."""
     lib = load_library()
+    flags = UAD_FLAG_ADARMS if getattr(shape, "conditioning", "input") == "adarms" else 0
     cfg = uad_model_config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
                            shape.d_ff, shape.action_dim, max_batch, max_chunk, max_prefix,
-                           float(shape.rms_eps), 0)
+                           float(shape.rms_eps), flags)
     if stream is None:
         stream = torch.cuda.current_stream(device)
     out = ctypes.c_void_p()

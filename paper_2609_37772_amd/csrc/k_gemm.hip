@@ -35,7 +35,7 @@ __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
 constexpr int kMaxTilesPerGroup = 4;
 
-template <int EPI, int T, int KPW>
+template <int EPI, int T, int KPW, bool DUAL>
 __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   extern __shared__ float red[];  // [waves][4*T*4 slots][64 lanes]
   __shared__ float rpart[8][64];  // partial sums of ssq for rstd
@@ -72,15 +72,18 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
     rpart[wave][lane] = acc;
   }
 
-  f32x4 acc[kMaxTilesPerGroup][T];
+  f32x4 acc[kMaxTilesPerGroup][T], acc2[kMaxTilesPerGroup][DUAL ? T : 1];
 #pragma unroll
-  for (int mt = 0; mt < kMaxTilesPerGroup; ++mt)
+  for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
 #pragma unroll
     for (int t = 0; t < T; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < (DUAL ? T : 1); ++t) acc2[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
   for (int pass = 0; pass < passes; ++pass) {
     const int kb0 = (pass * waves + wave) * KPW;
-    f16x8 w[KPW][T], a[KPW][kMaxTilesPerGroup];
+    f16x8 w[KPW][T], a[KPW][kMaxTilesPerGroup], a2[KPW][DUAL ? kMaxTilesPerGroup : 1];
     const op_t *wp = g.W + ((size_t)tile0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
     for (int j = 0; j < KPW; ++j)
@@ -92,6 +95,12 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       const bool ok = mt < nmt && (m0 + mt * 16 + (lane & 15)) < g.M;
 #pragma unroll
       for (int j = 0; j < KPW; ++j) a[j][mt] = ok ? *(const f16x8 *)(ap + ((size_t)mt * KB + j) * kBlockElems) : f16x8{};
+      if (DUAL) {
+        const op_t *ap2 = g.A2 + ((size_t)mt0 * KB + kb0) * kBlockElems + lane * 8;
+#pragma unroll
+        for (int j = 0; j < KPW; ++j)
+          a2[j][mt] = ok ? *(const f16x8 *)(ap2 + ((size_t)mt * KB + j) * kBlockElems) : f16x8{};
+      }
     }
 #pragma unroll
     for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
@@ -99,9 +108,33 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int j = 0; j < KPW; ++j)
 #pragma unroll
-        for (int t = 0; t < T; ++t)
+        for (int t = 0; t < T; ++t) {
           acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[j][mt], w[j][t], acc[mt][t], 0, 0, 0);
+          if (DUAL)
+            acc2[mt][DUAL ? t : 0] =
+                __builtin_amdgcn_mfma_f32_16x16x32_f16(a2[j][mt], w[j][t], acc2[mt][DUAL ? t : 0], 0, 0, 0);
+        }
     }
+  }
+
+  // Dual operand (normalised input = rstd * A + A2): fold rstd into each
+  // wave's partial tile before the cross-wave reduction (it is linear).
+  if (DUAL) {
+    __syncthreads();  // rpart complete
+    if (threadIdx.x < 64) {
+      float ss = 0.f;
+      for (int w2 = 0; w2 < waves; ++w2) ss += rpart[w2][threadIdx.x];
+      rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < kMaxTilesPerGroup; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float rs = rstd_s[mt * 16 + (lane >> 4) * 4 + r];
+#pragma unroll
+        for (int t = 0; t < T; ++t) acc[mt][t][r] = rs * acc[mt][t][r] + acc2[mt][DUAL ? t : 0][r];
+      }
   }
 
   // Cross-wave reduction through LDS, fixed order over waves.
@@ -113,7 +146,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[((wave * SLOTS) + (mt * T + t) * 4 + r) * 64 + lane] = acc[mt][t][r];
   __syncthreads();
-  if ((EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd && threadIdx.x < 64) {
+  if (!DUAL && (EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd && threadIdx.x < 64) {
     float ss = 0.f;
     for (int w2 = 0; w2 < waves; ++w2) ss += rpart[w2][threadIdx.x];
     rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
@@ -147,12 +180,35 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
     const int s0 = (mt * T + t) * 4 + r;
     float v = 0.f;
     for (int w2 = 0; w2 < waves; ++w2) v += red[(w2 * SLOTS + s0) * 64 + ln];
+    if (EPI == EPI_MOD) {
+      // column c: layer c / 6d, part (c % 6d) / d (0..5 = a, b, g of the
+      // attention norm, then of the MLP norm), index c % d; the final norm's
+      // (a, b) follow the layers
+      const int col = (tile0 + t) * 16 + (ln & 15);
+      if (row_ok) {
+        const float mv = v + g.bias[col];
+        ((float *)g.out)[(size_t)row * g.ldo + col] = mv;
+        const int per_layer = 6 * g.d_model;
+        const int l = col / per_layer;
+        if (l < g.n_layers) {
+          const int r6 = col - l * per_layer;
+          const int part = r6 / g.d_model, j = r6 - part * g.d_model;
+          const int KBd = g.d_model / kTileK;
+          if (part == 1 || part == 4)
+            store_op(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, j, KBd), mv);
+          else if (part == 0 && l == 0)
+            store_op(g.next + afrag_index(row, j, KBd), g.h_in[(size_t)row * g.d_model + j] * (1.0f + mv));
+        }
+      }
+      continue;
+    }
     if (EPI == EPI_RESID_F32) {
       const int col = (tile0 + t) * 16 + (ln & 15);
       float hv = 0.f;
       if (row_ok) {
         float *hp = (float *)g.out + (size_t)row * g.ldo + col;
-        hv = (g.bias ? g.bias[col] : *hp) + v;
+        const float gv = g.mod_gate ? g.mod_gate[(size_t)row * g.mod_ld + col] * v : v;
+        hv = (g.bias ? g.bias[col] : *hp) + gv;
         *hp = hv;
       }
       float sq = hv * hv;  // sum over the 16 columns of this row (lanes sharing ln>>4)
@@ -160,12 +216,16 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
       if (row_ok) {
         if ((ln & 15) == 0) g.ssq[(size_t)(tile0 + t) * g.m_alloc + row] = sq;
-        if (g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * g.gain_next[col]);
+        if (g.mod_scale_next)
+          store_op(g.next + afrag_index(row, col, g.N / kTileK),
+                   hv * (1.0f + g.mod_scale_next[(size_t)row * g.mod_ld + col]));
+        else if (g.gain_next)
+          store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * g.gain_next[col]);
       }
       continue;
     }
     if (!row_ok) continue;
-    const float rs = ((EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd) ? rstd_s[rl] : 1.0f;
+    const float rs = (!DUAL && (EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd) ? rstd_s[rl] : 1.0f;
     if (EPI == EPI_GEGLU) {
       const int s1 = (mt * T + t + 1) * 4 + r;
       float u = 0.f;
@@ -203,7 +263,14 @@ template <int EPI, int T, int KPW>
 static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   dim3 grid(g.N / kTileN / T, 1, p.mgroups);
   const uint32_t lds = (uint32_t)(p.waves * kMaxTilesPerGroup * T * 4 * 64 * sizeof(float));
-  UAD_LAUNCH((gemm_kernel<EPI, T, KPW>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
+  if constexpr (EPI == EPI_QKV || EPI == EPI_GEGLU) {
+    if (g.A2) {
+      if (!g.use_rstd) return hipErrorInvalidValue;
+      UAD_LAUNCH((gemm_kernel<EPI, T, KPW, true>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
+      return hipGetLastError();
+    }
+  }
+  UAD_LAUNCH((gemm_kernel<EPI, T, KPW, false>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
 
@@ -215,7 +282,7 @@ static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, 
 GemmPlan plan_gemm(int epi, int M, int N, int K) {
   GemmPlan p{};
   const int KB = K / kTileK;
-  p.T = (epi == EPI_GEGLU) ? 2 : 1;
+  p.T = (epi == EPI_GEGLU || epi == EPI_MOD) ? 2 : 1;
   const int ngroups = N / kTileN / p.T;
   const int MT = (M + 15) / 16;
   if (MT > kMaxTilesPerGroup) {
@@ -254,6 +321,7 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
     case EPI_RESID_F32: UAD_GEMM_KPW_CASES(EPI_RESID_F32, 1)
     case EPI_GEGLU: UAD_GEMM_KPW_CASES(EPI_GEGLU, 2)
     case EPI_QKV: UAD_GEMM_KPW_CASES(EPI_QKV, 1)
+    case EPI_MOD: UAD_GEMM_KPW_CASES(EPI_MOD, 2)
   }
   return hipErrorInvalidValue;
 }

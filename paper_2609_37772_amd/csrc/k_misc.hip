@@ -44,6 +44,40 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
   }
 }
 
+// Adaptive-norm variant: te[m] = e(t_m) alone (K = d) as the time MLP's fp16
+// operand; the action token itself starts the residual stream,
+// h[m] = x_m W_in^T + b_in (fp32), with its per-16-column sums of squares.
+__global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__ x, const float *__restrict__ t,
+                                                        int Da, int d, const float *__restrict__ w_in,
+                                                        const float *__restrict__ b_in,
+                                                        const float *__restrict__ freqs, op_t *__restrict__ te,
+                                                        float *__restrict__ h, float *__restrict__ ssq,
+                                                        int m_alloc) {
+  __shared__ float xs[64];
+  const int m = blockIdx.x;
+  const int KB = d / kTileK;
+  if (threadIdx.x < Da) xs[threadIdx.x] = x[(size_t)m * Da + threadIdx.x];
+  __syncthreads();
+  // d is a multiple of 32, so the 16 lanes of a 16-column tile are active together
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    float acc = b_in[n];
+    const float *w = w_in + (size_t)n * Da;
+    for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
+    h[(size_t)m * d + n] = acc;
+    float sq = acc * acc;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
+    if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
+  }
+  const float tm = t[m];
+  const int half = d >> 1;
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    const float arg = freqs[j] * tm;
+    store_op(te + afrag_index(m, j, KB), sinf(arg));
+    store_op(te + afrag_index(m, half + j, KB), cosf(arg));
+  }
+}
+
 // v = RMSNorm(h) W_out^T + b_out, then x <- x + dt v unless frozen (mask or
 // dt == 0: copy, so frozen tokens are bit-identical whatever v holds).
 // Workgroup = (token m, group of up to 8 action dims); thread t owns columns
@@ -63,19 +97,22 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
       vs[threadIdx.x] = f.dbg_alpha * f.x[(size_t)m * f.Da + a0 + threadIdx.x] + f.dbg_beta;
   } else {
     const float *__restrict__ hr = f.h + (size_t)m * d;
-    float hv[NC], gv[NC], wv[kFinalOuts][NC];
+    float hv[NC], gv[NC], sv[NC], wv[kFinalOuts][NC];
+    const bool ada = f.mod_scale != nullptr;
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
       const int c = min(threadIdx.x + 256 * i, d - 1);
       hv[i] = hr[c];
-      gv[i] = f.gain[c];
+      // adaptive norm: per-token scale (1 + a) and shift b; else the gain
+      gv[i] = ada ? 1.0f + f.mod_scale[(size_t)m * f.mod_ld + c] : f.gain[c];
+      sv[i] = ada ? f.mod_shift[(size_t)m * f.mod_ld + c] : 0.f;
 #pragma unroll
       for (int o = 0; o < kFinalOuts; ++o) wv[o][i] = f.w_out[(size_t)min(a0 + o, f.Da - 1) * d + c];
     }
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
-      if (threadIdx.x + 256 * i >= d) hv[i] = 0.f;
+      if (threadIdx.x + 256 * i >= d) hv[i] = sv[i] = 0.f;  // clamped duplicate columns contribute nothing
       ss += hv[i] * hv[i];
     }
     ss = block_sum_256(ss, scratch);
@@ -85,7 +122,7 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
     for (int o = 0; o < kFinalOuts; ++o) {
       acc[o] = 0.f;
 #pragma unroll
-      for (int i = 0; i < NC; ++i) acc[o] += (hv[i] * rstd * gv[i]) * wv[o][i];
+      for (int i = 0; i < NC; ++i) acc[o] += (hv[i] * rstd * gv[i] + sv[i]) * wv[o][i];
 #pragma unroll
       for (int off = 32; off >= 1; off >>= 1) acc[o] += __shfl_xor(acc[o], off);
     }
@@ -175,6 +212,14 @@ hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, con
                        const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
   UAD_LAUNCH(temb_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te);
+  return hipGetLastError();
+}
+
+hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
+                           const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
+                           hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  UAD_LAUNCH(temb_ada_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, h, ssq,
+             m_alloc);
   return hipGetLastError();
 }
 

@@ -109,9 +109,9 @@ struct Carve {
 
 // Kernel classes reported by the measurement hook.
 enum KClass { K_TEMB, K_GEMM_TIME_IN, K_GEMM_TIME_OUT, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP,
-              K_GEMM_DOWN, K_FINAL, K_NCLASS };
+              K_GEMM_DOWN, K_FINAL, K_GEMM_MOD, K_NCLASS };
 const char *kClassNames[K_NCLASS] = {"temb", "gemm_time_in", "gemm_time_out", "gemm_qkv", "attention",
-                                     "gemm_o", "gemm_gateup", "gemm_down", "final_euler"};
+                                     "gemm_o", "gemm_gateup", "gemm_down", "final_euler", "gemm_mod"};
 
 hipEvent_t pool_event(uad_ctx *c) {
   if (!c->ev_pool.empty()) {
@@ -158,7 +158,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   if (m.n_layers < 1 || m.d_model < 1 || m.n_heads < 1 || m.n_kv_heads < 1 || m.head_dim < 1 || m.d_ff < 1 ||
       m.action_dim < 1 || m.max_batch < 1 || m.max_chunk < 1 || m.max_prefix < 0 || !(m.rms_eps >= 0.f))
     return cerr(UAD_E_INVALID, "uad_create: every dimension must be positive");
-  if (m.flags != 0) return cerr(UAD_E_INVALID, "uad_create: flags must be 0");
+  if ((m.flags & ~UAD_FLAG_ADARMS) != 0) return cerr(UAD_E_INVALID, "uad_create: unknown flags");
   if (m.d_model % 32 || m.d_ff % 32) return cerr(UAD_E_UNSUPPORTED, "uad_create: d_model and d_ff must be multiples of 32");
   if (m.head_dim != 64 && m.head_dim != 128 && m.head_dim != 256)
     return cerr(UAD_E_UNSUPPORTED, "uad_create: head_dim must be 64, 128 or 256");
@@ -183,6 +183,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->kv_dim = c->Hkv * c->hd;
   c->n_qkv = c->q_dim + 2 * c->kv_dim;
   c->m_alloc = round_up(m.max_batch * m.max_chunk, 64);
+  c->ada = (m.flags & UAD_FLAG_ADARMS) != 0;
+  c->n_mod = c->ada ? m.n_layers * 6 * m.d_model + 2 * m.d_model : 0;
   c->s_alloc = round_up(m.max_prefix + m.max_chunk, 32);
   c->layers.resize(c->L);
 
@@ -207,8 +209,9 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   Carve w;
   size_t o_ain = w.take<float>((size_t)d * Da), o_ainb = w.take<float>(d), o_t1b = w.take<float>(d),
          o_t2b = w.take<float>(d), o_fn = w.take<float>(d), o_aout = w.take<float>((size_t)Da * d),
-         o_aoutb = w.take<float>(Da), o_freq = w.take<float>(d / 2), o_t1 = w.take<uint16_t>((size_t)d * 2 * d),
-         o_t2 = w.take<uint16_t>((size_t)d * d);
+         o_aoutb = w.take<float>(Da), o_freq = w.take<float>(d / 2),
+         o_t1 = w.take<uint16_t>((size_t)d * (c->ada ? d : 2 * d)), o_t2 = w.take<uint16_t>((size_t)d * d),
+         o_wmod = w.take<uint16_t>((size_t)c->n_mod * d), o_bmod = w.take<float>(c->n_mod);
   std::vector<size_t> o_l(6 * c->L);
   for (int l = 0; l < c->L; ++l) {
     o_l[6 * l + 0] = w.take<uint16_t>((size_t)c->n_qkv * d);
@@ -235,6 +238,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->freqs = (float *)(wb + o_freq);
   c->t1_w = (op_t *)(wb + o_t1);
   c->t2_w = (op_t *)(wb + o_t2);
+  c->w_mod = (op_t *)(wb + o_wmod);
+  c->b_mod = (float *)(wb + o_bmod);
   for (int l = 0; l < c->L; ++l) {
     c->layers[l].wqkv = (const op_t *)(wb + o_l[6 * l + 0]);
     c->layers[l].wo = (const op_t *)(wb + o_l[6 * l + 1]);
@@ -287,7 +292,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
          o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
          o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M),
          o_trx0 = a.take<float>(M * Da), o_trv = a.take<float>(M * Da), o_trt = a.take<float>(kMaxTrSteps * M),
-         o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M);
+         o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M),
+         o_mod = a.take<float>(M * c->n_mod), o_mshift = a.take<uint16_t>(c->ada ? (size_t)2 * c->L * M * d : 0);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -310,6 +316,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->tr_t = (float *)(ab + o_trt);
   c->tr_dt = (float *)(ab + o_trdt);
   c->tr_mask = (uint8_t *)(ab + o_trm);
+  c->mod = (float *)(ab + o_mod);
+  c->mod_shift_ops = (op_t *)(ab + o_mshift);
   e = attention_init();
   if (e != hipSuccess) {
     uad_destroy(c);
@@ -377,21 +385,33 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
   std::map<std::string, std::vector<int64_t>> need;
   need["action_in.w"] = {d, Da};
   need["action_in.b"] = {d};
-  need["time_mlp_in.w"] = {d, 2 * d};
+  need["time_mlp_in.w"] = {d, c->ada ? d : 2 * d};
   need["time_mlp_in.b"] = {d};
   need["time_mlp_out.w"] = {d, d};
   need["time_mlp_out.b"] = {d};
-  need["final_norm"] = {d};
+  if (c->ada) {
+    need["final_mod.w"] = {2 * d, d};
+    need["final_mod.b"] = {2 * d};
+  } else {
+    need["final_norm"] = {d};
+  }
   need["action_out.w"] = {Da, d};
   need["action_out.b"] = {Da};
   for (int l = 0; l < c->L; ++l) {
     const std::string p = "layers." + std::to_string(l) + ".";
-    need[p + "attn_norm"] = {d};
+    if (c->ada) {
+      need[p + "attn_mod.w"] = {3 * d, d};
+      need[p + "attn_mod.b"] = {3 * d};
+      need[p + "mlp_mod.w"] = {3 * d, d};
+      need[p + "mlp_mod.b"] = {3 * d};
+    } else {
+      need[p + "attn_norm"] = {d};
+      need[p + "mlp_norm"] = {d};
+    }
     need[p + "wq"] = {c->q_dim, d};
     need[p + "wk"] = {c->kv_dim, d};
     need[p + "wv"] = {c->kv_dim, d};
     need[p + "wo"] = {d, c->q_dim};
-    need[p + "mlp_norm"] = {d};
     need[p + "w_gate"] = {F, d};
     need[p + "w_up"] = {F, d};
     need[p + "w_down"] = {d, F};
@@ -434,11 +454,12 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
   };
   bool ok = put_f32("action_in.w", c->action_in_w) && put_f32("action_in.b", c->action_in_b) &&
             put_f32("time_mlp_in.b", c->t1_b) && put_f32("time_mlp_out.b", c->t2_b) &&
-            put_f32("final_norm", c->final_norm) && put_f32("action_out.w", c->action_out_w) &&
+            (c->ada || put_f32("final_norm", c->final_norm)) && put_f32("action_out.w", c->action_out_w) &&
             put_f32("action_out.b", c->action_out_b);
+  const int k_t1 = c->ada ? d : 2 * d;
   if (ok && (ok = host("time_mlp_in.w", &v1))) {
-    pk.assign((size_t)d * 2 * d, 0);
-    range_ok &= pack_tiles(v1.data(), d, 2 * d, pk.data(), 0, 1);
+    pk.assign((size_t)d * k_t1, 0);
+    range_ok &= pack_tiles(v1.data(), d, k_t1, pk.data(), 0, 1);
     ok = up(c->t1_w, pk.data(), pk.size() * 2);
   }
   if (ok && (ok = host("time_mlp_out.w", &v1))) {
@@ -449,8 +470,10 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
   for (int l = 0; ok && l < c->L; ++l) {
     const std::string p = "layers." + std::to_string(l) + ".";
     uad_layer_ptrs &lp = c->layers[l];
-    ok = put_f32(p + "attn_norm", (float *)lp.attn_norm) && put_f32(p + "mlp_norm", (float *)lp.mlp_norm);
-    if (!ok) break;
+    if (!c->ada) {
+      ok = put_f32(p + "attn_norm", (float *)lp.attn_norm) && put_f32(p + "mlp_norm", (float *)lp.mlp_norm);
+      if (!ok) break;
+    }
     // fused QKV: tiles [q | k | v]
     pk.assign((size_t)c->n_qkv * d, 0);
     ok = host(p + "wq", &v1) && host(p + "wk", &v2) && host(p + "wv", &v3);
@@ -479,6 +502,29 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
     pk.assign((size_t)d * F, 0);
     range_ok &= pack_tiles(v1.data(), d, F, pk.data(), 0, 1);
     ok = up((void *)lp.wdown, pk.data(), pk.size() * 2);
+  }
+  if (ok && c->ada) {
+    // all modulations in one matrix [n_mod][d]: per layer (a, b, g) of the
+    // attention norm, (a, b, g) of the MLP norm; then (a, b) of the final norm
+    pk.assign((size_t)c->n_mod * d, 0);
+    std::vector<float> bm(c->n_mod);
+    const int per_layer_tiles = 6 * d / kTileN;
+    for (int l = 0; ok && l < c->L; ++l) {
+      const std::string p = "layers." + std::to_string(l) + ".";
+      ok = host(p + "attn_mod.w", &v1) && host(p + "mlp_mod.w", &v2) && host(p + "attn_mod.b", &v3);
+      if (!ok) break;
+      range_ok &= pack_tiles(v1.data(), 3 * d, d, pk.data(), l * per_layer_tiles, 1);
+      range_ok &= pack_tiles(v2.data(), 3 * d, d, pk.data(), l * per_layer_tiles + 3 * d / kTileN, 1);
+      std::copy(v3.begin(), v3.end(), bm.begin() + (size_t)l * 6 * d);
+      ok = host(p + "mlp_mod.b", &v3);
+      if (!ok) break;
+      std::copy(v3.begin(), v3.end(), bm.begin() + (size_t)l * 6 * d + 3 * d);
+    }
+    if (ok && (ok = host("final_mod.w", &v1) && host("final_mod.b", &v3))) {
+      range_ok &= pack_tiles(v1.data(), 2 * d, d, pk.data(), c->L * per_layer_tiles, 1);
+      std::copy(v3.begin(), v3.end(), bm.begin() + (size_t)c->L * 6 * d);
+      ok = up(c->w_mod, pk.data(), pk.size() * 2) && up(c->b_mod, bm.data(), bm.size() * 4);
+    }
   }
   if (!ok) {
     c->weights_loaded = false;
@@ -574,22 +620,42 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     if (c->prof_on) c->prof_pending.push_back({cls, ea_, eb_}); \
   } while (0)
   if (!c->dbg) {
-    UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, s,
-                                      ea_, eb_));
     // RMSNorm folding: residual GEMMs write ssq and the next operand; consumers scale by rstd
     auto norm_fields = [&](GemmArgs &x) {
       x.ssq = c->ssq; x.ssq_tiles = d / 16; x.m_alloc = (int)MA; x.eps = c->cfg.rms_eps;
     };
-    GemmArgs g{};
-    g.M = M;
-    g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = 2 * d;
-    g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
-    UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, 2 * d), s, ea_, eb_));
-    GemmArgs g2{};
-    g2.M = M; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d;
-    g2.out = c->h; g2.ldo = d; g2.bias = c->t2_b; norm_fields(g2);
-    g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n;
-    UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_RESID_F32, g2, plan_gemm(EPI_RESID_F32, M, d, d), s, ea_, eb_));
+    const int n_mod = c->n_mod;
+    if (!c->ada) {
+      UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, s,
+                                        ea_, eb_));
+      GemmArgs g{};
+      g.M = M;
+      g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = 2 * d;
+      g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
+      UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, 2 * d), s, ea_, eb_));
+      GemmArgs g2{};
+      g2.M = M; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d;
+      g2.out = c->h; g2.ldo = d; g2.bias = c->t2_b; norm_fields(g2);
+      g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n;
+      UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_RESID_F32, g2, plan_gemm(EPI_RESID_F32, M, d, d), s, ea_, eb_));
+    } else {
+      // adaptive norms: h_0 = W_in x + b_in, c = SiLU(W2 SiLU(W1 e(t) + b1) + b2), then every
+      // modulation (a, b, g per norm site) in one GEMM whose epilogue also forms the
+      // first attention norm's operand h_0 * (1 + a)
+      UAD_CHECK_CLS(K_TEMB, launch_temb_ada(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
+                                            c->h, c->ssq, (int)MA, s, ea_, eb_));
+      GemmArgs g{};
+      g.M = M; g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = d; g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
+      UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, d), s, ea_, eb_));
+      GemmArgs g2{};
+      g2.M = M; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d; g2.out = c->a_te; g2.ldo = d; g2.bias = c->t2_b;
+      UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_SILU, g2, plan_gemm(EPI_BIAS_SILU, M, d, d), s, ea_, eb_));
+      GemmArgs gm{};
+      gm.M = M; gm.A = c->a_te; gm.W = c->w_mod; gm.N = n_mod; gm.K = d; gm.out = c->mod; gm.ldo = n_mod;
+      gm.bias = c->b_mod; gm.mod_shift_ops = c->mod_shift_ops; gm.shift_stride = MA * d; gm.h_in = c->h;
+      gm.d_model = d; gm.n_layers = c->L; gm.next = c->a_n;
+      UAD_CHECK_CLS(K_GEMM_MOD, launch_gemm(EPI_MOD, gm, plan_gemm(EPI_MOD, M, n_mod, d), s, ea_, eb_));
+    }
 
     AttnArgs at{};
     at.q = c->q; at.ldq = c->q_dim; at.s_alloc = c->s_alloc; at.n_keys = c->prefix_len + H;
@@ -612,6 +678,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
       norm_fields(q); q.use_rstd = 1;
+      if (c->ada) q.A2 = c->mod_shift_ops + (size_t)(2 * l) * MA * d;
       UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, pq, s, ea_, eb_));
       at.kc = kc; at.vtc = vtc;
       UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s, ea_, eb_));
@@ -619,15 +686,25 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       o.M = M; o.A = c->a_o; o.W = lp.wo; o.N = d; o.K = c->q_dim;
       o.out = c->h; o.ldo = d; norm_fields(o);
       o.gain_next = lp.mlp_norm; o.next = c->a_n;
+      if (c->ada) {
+        const float *ml = c->mod + (size_t)l * 6 * d;
+        o.mod_ld = n_mod; o.mod_gate = ml + 2 * d; o.mod_scale_next = ml + 3 * d; o.gain_next = nullptr;
+      }
       UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, po, s, ea_, eb_));
       GemmArgs gu{};
       gu.M = M; gu.A = c->a_n; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
       gu.out = c->a_g; gu.ldo = F; norm_fields(gu); gu.use_rstd = 1;
+      if (c->ada) gu.A2 = c->mod_shift_ops + (size_t)(2 * l + 1) * MA * d;
       UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU, gu, pg, s, ea_, eb_));
       GemmArgs dn{};
       dn.M = M; dn.A = c->a_g; dn.W = lp.wdown; dn.N = d; dn.K = F;
       dn.out = c->h; dn.ldo = d; norm_fields(dn);
       dn.gain_next = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr; dn.next = c->a_n;
+      if (c->ada) {
+        const float *ml = c->mod + (size_t)l * 6 * d;
+        dn.mod_ld = n_mod; dn.mod_gate = ml + 5 * d; dn.gain_next = nullptr;
+        dn.mod_scale_next = (l + 1 < c->L) ? ml + 6 * d : nullptr;
+      }
       UAD_CHECK_CLS(K_GEMM_DOWN, launch_gemm(EPI_RESID_F32, dn, pd, s, ea_, eb_));
     }
   }
@@ -637,6 +714,9 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
   f.is_last_step = is_last; f.step = step; f.v_out = v_out; f.released = released; f.release_step = release_step;
   f.debug_field = c->dbg ? 1 : 0; f.dbg_alpha = c->dbg_alpha; f.dbg_beta = c->dbg_beta;
   f.vsum = vsum; f.vsum_tokens = vsum_tokens; f.chunk = H;
+  if (c->ada) {
+    f.mod_scale = c->mod + (size_t)c->L * 6 * d; f.mod_shift = f.mod_scale + d; f.mod_ld = c->n_mod;
+  }
   UAD_CHECK_CLS(K_FINAL, launch_final(f, s, ea_, eb_));
 #undef UAD_CHECK_CLS
   return UAD_OK;

@@ -82,7 +82,8 @@ enum Epilogue : int {
   EPI_BIAS_SILU = 0,   // out = fp16 silu(acc + bias), fragment order
   EPI_RESID_F32 = 1,   // h = (bias | h) + acc; per-tile sum of squares; next operand fp16(h * gain_next)
   EPI_GEGLU = 3,       // out = fp16 gelu_tanh(rstd*acc_gate) * rstd*acc_up (interleaved gate/up)
-  EPI_QKV = 4,             // rstd*acc: q -> bf16 q buffer; k, v -> per-layer K / V^T store
+  EPI_QKV = 4,         // rstd*acc: q -> bf16 q buffer; k, v -> per-layer K / V^T store
+  EPI_MOD = 5,         // adaptive-norm modulations of every norm site (see uad_ctx::mod)
 };
 
 struct GemmPlan {
@@ -105,6 +106,17 @@ struct GemmArgs {
   const float *gain_next; // EPI_RESID_F32: gain of the following RMSNorm (nullptr: none)
   op_t *next;             // EPI_RESID_F32: next operand, fragment order (K = N)
   int use_rstd;           // EPI_QKV / EPI_GEGLU: scale by rstd from ssq
+  // adaptive-norm conditioning
+  const op_t *A2;         // EPI_QKV / EPI_GEGLU: second operand (the norm's shift), result rstd*(A W) + A2 W
+  const float *mod_gate;  // EPI_RESID_F32: h += gate[row * mod_ld + col] * acc (nullptr: gate 1)
+  const float *mod_scale_next;  // EPI_RESID_F32: next operand fp16(h * (1 + scale[row * mod_ld + col]))
+  int mod_ld;
+  // EPI_MOD destinations: fp32 [M][N] row-major (out), the shifts as fp16
+  // operands, and the first attention norm's operand fp16(h * (1 + scale))
+  op_t *mod_shift_ops;    // [L][2][m_alloc*d] fragment order
+  const float *h_in;      // [M][d] residual stream
+  int d_model, n_layers;
+  size_t shift_stride;    // elements per shift operand
   const op_t *W;    // packed weights, N/16 tiles x K/32 blocks
   int M, N, K;      // N counts packed output columns (2F for gate/up)
   void *out;        // epilogue destination
@@ -150,6 +162,9 @@ struct FinalArgs {
   int32_t *release_step;// [M] or null
   int debug_field;
   float dbg_alpha, dbg_beta;
+  // adaptive-norm conditioning of the final norm: RMS(h) * (1 + scale) + shift
+  const float *mod_scale, *mod_shift;  // [M][mod_ld] or null (then the gain applies)
+  int mod_ld;
   // Trajectory Reconciliation: vsum[m] += v for tokens (m % chunk) < vsum_tokens
   float *vsum;          // [M][Da] or null
   int vsum_tokens, chunk;
@@ -185,6 +200,11 @@ int attention_max_splits(int head_dim);    // split-KV partials the combine acce
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                        const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// adaptive-norm variant: te <- e(t) (K = d); h <- W_in x + b_in with its
+// per-16-column sums of squares ssq[d/16][m_alloc]
+hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
+                           const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
+                           hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
 hipError_t launch_tr_init(const TrArgs &a, hipStream_t s);     // x0 <- x, vsum <- 0
@@ -227,7 +247,7 @@ struct GraphKey {
 
 struct uad_layer_ptrs {
   const uad::op_t *wqkv, *wo, *wgu, *wdown;
-  const float *attn_norm, *mlp_norm;
+  const float *attn_norm, *mlp_norm;  // input conditioning only
 };
 
 struct uad_ctx {
@@ -265,6 +285,14 @@ struct uad_ctx {
   size_t attn_part_elems = 0;
   float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]
   void *abuf = nullptr;
+
+  // adaptive-norm conditioning (flag UAD_FLAG_ADARMS)
+  bool ada = false;
+  int n_mod = 0;                      // L*6d + 2d modulation columns
+  uad::op_t *w_mod = nullptr;         // packed [n_mod][d]
+  float *b_mod = nullptr;             // [n_mod]
+  float *mod = nullptr;               // [m_alloc][n_mod] per token: per layer (a,b,g)_attn (a,b,g)_mlp, then (a,b)_final
+  uad::op_t *mod_shift_ops = nullptr; // [L][2][m_alloc*d] shifts as fp16 operands
 
   // urgency-aware release with Trajectory Reconciliation
   float *tr_x0 = nullptr, *tr_vsum = nullptr;  // [m_alloc][Da]

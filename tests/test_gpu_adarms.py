@@ -1,0 +1,95 @@
+"""GPU parity of the adaptive-norm-conditioned expert (App. C.1, the
+pi0.5-style variant: the per-token time modulates every RMSNorm and gates
+every residual branch) against the oracle, through the C ABI.
+
+Bars as for the input-conditioned expert: per-step velocities within a
+normwise max relative error of 2e-2 (teacher-forced), final and released
+actions within 1e-2 absolute (free-running schedule), release steps
+bit-exact; the release path (TR, K = 1) reproduces the uniform schedule bit
+for bit on this model too.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from tests.harness import log, make_case, rel_err
+
+pytestmark = pytest.mark.gpu
+
+VEL_RTOL = 2e-2
+ACT_ATOL = 1e-2
+_cases = {}
+
+
+def case(name, **kw):
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cases:
+        _cases[key] = make_case(name, **kw)
+    return _cases[key]
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.mark.parametrize("name,steps", [("tiny_adarms", None), ("pi05_b1_adarms", [0, 4, 9])])
+def test_adarms_teacher_forced_velocity(gpu, name, steps):
+    c = case(name)
+    r = O.denoise_schedule(c.oracle_model(), c.noise, c.budgets, keep_history=True)
+    for k in (range(r["n_steps"]) if steps is None else steps):
+        x_in, v_ref = r["history"][k]
+        xg = dev(x_in.astype(np.float32))
+        vg = torch.empty_like(xg)
+        c.expert.step(xg, dev(r["t"][k].astype(np.float32)), dev(r["dt"][k].astype(np.float32)),
+                      dev(r["mask"][k].astype(np.uint8)), vg)
+        torch.cuda.synchronize()
+        e = rel_err(vg.cpu().numpy()[0], v_ref[0])
+        log(f"[{name}] step {k}: velocity rel err {e:.2e}")
+        assert e <= VEL_RTOL
+
+
+@pytest.mark.parametrize("name", ["tiny_adarms", "pi05_b1_adarms"])
+def test_adarms_free_running_uad_schedule(gpu, name):
+    """Budgets 4 / 7 / 10 over the chunk: per-token flow times reach the norms."""
+    c = case(name)
+    H = c.wl.chunk
+    bud = np.full((1, H), 10, np.int32)
+    bud[0, : H // 10] = 4
+    bud[0, H // 10: H // 2] = 7
+    r = O.denoise_schedule(c.oracle_model(), c.noise, bud)
+    n, tg, dtg, mg = c.expert.schedule_tables(bud)
+    x = dev(c.noise.astype(np.float32))
+    rel = torch.zeros_like(x)
+    rst = torch.full(bud.shape, -1, dtype=torch.int32, device="cuda")
+    c.expert.schedule(x, tg, dtg, mg, rel, rst)
+    torch.cuda.synchronize()
+    ex, er = np.abs(x.cpu().numpy() - r["x"]).max(), np.abs(rel.cpu().numpy() - r["released"]).max()
+    log(f"[{name}] final max abs err {ex:.2e}, released {er:.2e}")
+    assert ex <= ACT_ATOL and er <= ACT_ATOL
+    np.testing.assert_array_equal(rst.cpu().numpy(), r["release_step"])
+
+
+def test_adarms_tr_k1_bit_exact(gpu):
+    c = case("tiny_adarms")
+    x = dev(c.noise.astype(np.float32))
+    c.expert.release(x, 5, 1, 7, 10)
+    n, tg, dtg, mg = c.expert.schedule_tables(np.full((1, c.wl.chunk), 7, np.int32))
+    xv = dev(c.noise.astype(np.float32))
+    c.expert.schedule(xv, tg, dtg, mg)
+    torch.cuda.synchronize()
+    assert torch.equal(x, xv)
+
+
+def test_adarms_time_changes_velocity(gpu):
+    """Time must reach the output through the modulations: same x, different t."""
+    c = case("tiny_adarms")
+    H, Da = c.wl.chunk, c.wl.shape.action_dim
+    vs = []
+    for tv in (1.0, 0.3):
+        xg = dev(c.noise.astype(np.float32))
+        vg = torch.empty_like(xg)
+        c.expert.step(xg, torch.full((1, H), tv, device="cuda"), torch.zeros((1, H), device="cuda"),
+                      torch.zeros((1, H), dtype=torch.uint8, device="cuda"), vg)
+        vs.append(vg.cpu().numpy())
+    assert np.abs(vs[0] - vs[1]).max() > 1e-3

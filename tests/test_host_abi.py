@@ -77,7 +77,7 @@ def _cfg(uad, **kw):
 
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 96, 7), ("d_model", 48, 7), ("n_kv_heads", 3, 7), ("action_dim", 65, 7),
-    ("n_layers", 0, 1), ("max_batch", 0, 1), ("flags", 1, 1),
+    ("n_layers", 0, 1), ("max_batch", 0, 1), ("flags", 2, 1), ("flags", -1, 1),
 ])
 def test_create_validates_before_device_work(uad, field, value, status):
     lib = uad.load_library()
