@@ -136,6 +136,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-aal", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the run, copy an MIB-MiB fp32 buffer 3 times (a plain copy kernel of known "
+                         "size, the reference for hardware byte counters)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the hot path is measured on one "
@@ -274,6 +277,14 @@ def main():
         out["cpu_baseline"] = cpu_baseline(wl, weights, prefix, noise, budgets, a.cpu_seconds)
         one = cpu_baseline(wl, weights, prefix, noise, budgets, a.cpu_seconds / 2, limit_threads=1)
         out["cpu_baseline_1thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
+    if a.copy_calibration > 0:
+        n = a.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration"] = {"bytes_read": n * 4, "bytes_written": n * 4, "launches": 3}
     print(json.dumps(out), flush=True)
     ex.close()
 

@@ -61,9 +61,16 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int INS = HD / 64;  // LDS-direct instructions per wave per tile (4 waves x 64 lanes x 16 B)
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int qblock = blockIdx.x;
-  const int split = blockIdx.y;
-  const int eh = blockIdx.z;  // env * Hkv + kv head
+  // XCD-aware placement: the query blocks of one (environment-head, split)
+  // group read the same K/V tiles, so the group's workgroups get ids on one
+  // XCD (workgroup i runs on XCD i % 8) and share its L2; groups are dealt
+  // round-robin over the 8 XCDs.
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int rgrp = slot / a.qblocks, qblock = slot - rgrp * a.qblocks;
+  const int grp = xcd + 8 * rgrp;
+  if (grp >= a.n_eh * a.splits) return;  // padding of the last round (whole workgroup)
+  const int eh = grp / a.splits;  // env * Hkv + kv head
+  const int split = grp - eh * a.splits;
   const int b = eh / a.n_kv_heads;
   const int g = eh - b * a.n_kv_heads;
 
@@ -199,11 +206,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   l_tot += __shfl_xor(l_tot, 16);
   l_tot += __shfl_xor(l_tot, 32);
 
-  if (a.splits == 1) {
-    // Output rows of this lane: r0 + 4*(lane>>4) + r, column 16*nt + (lane&15)
-    float lr[4];
+  // Output rows of this lane: r0 + 4*(lane>>4) + r, column 16*nt + (lane&15)
+  float lr[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) lr[r] = __shfl(l_tot, (lane >> 4) * 4 + r);
+  for (int r = 0; r < 4; ++r) lr[r] = __shfl(l_tot, (lane >> 4) * 4 + r);
+  if (a.splits == 1) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = r0 + (lane >> 4) * 4 + r;
@@ -217,19 +224,27 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv);
     }
   } else {
-    // Partials in the accumulator's own layout: per 16-row tile, [nt][lane][4]
-    // floats (one 16-byte store per lane and column tile), and (m, l) per row.
-    const size_t tile = ((size_t)split * gridDim.z + eh) * (a.rows_pad / 16) + (r0 >> 4);
-    float *op = a.opart + tile * (16 * HD) + lane * 4;
+    // Partials o_s / l_s in fp16 (bounded by max |V|), in the accumulator's
+    // own layout: per 16-row tile, [nt][lane][4] (one 8-byte store per lane and
+    // column tile), and (m, l) per row in fp32.
+    const size_t tile = ((size_t)split * a.n_eh + eh) * (a.rows_pad / 16) + (r0 >> 4);
+    op_t *op = a.opart + tile * (16 * HD) + lane * 4;
+    float inv[4];
 #pragma unroll
-    for (int nt = 0; nt < NTO; ++nt) *(f32x4 *)(op + nt * 256) = o[nt];
+    for (int r = 0; r < 4; ++r) inv[r] = 1.0f / lr[r];
+#pragma unroll
+    for (int nt = 0; nt < NTO; ++nt) {
+      typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
+      *(f16x4 *)(op + nt * 256) = f16x4{(op_t)(o[nt][0] * inv[0]), (op_t)(o[nt][1] * inv[1]),
+                                         (op_t)(o[nt][2] * inv[2]), (op_t)(o[nt][3] * inv[3])};
+    }
     // lanes 0..15 hold the statistics of their own query row r0 + lane
     if (lane < 16) *(float2 *)(a.mlpart + (tile * 16 + lane) * 2) = float2{m_run, l_tot};
   }
 }
 
-// Merge split-KV partials: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
-// splits in fixed order.  One wave per (16-row tile, 16-column tile): lane l
+// Merge split-KV partials: with o_s = O_s / l_s stored,
+// o = sum_s 2^(m_s - M) l_s o_s / sum_s 2^(m_s - M) l_s, splits in fixed order.  One wave per (16-row tile, 16-column tile): lane l
 // owns the float4 of the accumulator layout (rows 4*(l>>4)..+3, column l&15)
 // and reads the (m, l) pairs of its 4 rows itself, so all loads are issued
 // up front and the merge needs no LDS or barrier.
@@ -244,13 +259,14 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
   const int ntiles = a.rows_pad / 16;
   const int lane = threadIdx.x;
   const int rbase = (lane >> 4) * 4;
-  f32x4 os[SMAX];
+  typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
+  f16x4 os[SMAX];
   float2 ml[SMAX][4];
 #pragma unroll
   for (int sp = 0; sp < SMAX; ++sp) {
     const size_t tile = ((size_t)min(sp, splits - 1) * n_eh + eh) * ntiles + rt;
-    const f32x4 ov = *(const f32x4 *)(a.opart + tile * (16 * (size_t)hd) + nt * 256 + lane * 4);
-    os[sp] = sp < splits ? ov : f32x4{};
+    const f16x4 ov = *(const f16x4 *)(a.opart + tile * (16 * (size_t)hd) + nt * 256 + lane * 4);
+    os[sp] = sp < splits ? ov : f16x4{};
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const float2 v = *(const float2 *)(a.mlpart + (tile * 16 + rbase + r) * 2);
@@ -265,9 +281,9 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
     float num = 0.f, den = 0.f;
 #pragma unroll
     for (int sp = 0; sp < SMAX; ++sp) {
-      const float w = sp < splits ? __builtin_amdgcn_exp2f(ml[sp][r].x - M) : 0.f;
-      num += w * os[sp][r];
-      den += w * ml[sp][r].y;
+      const float w = sp < splits ? __builtin_amdgcn_exp2f(ml[sp][r].x - M) * ml[sp][r].y : 0.f;
+      num += w * (float)os[sp][r];
+      den += w;
     }
     const int row = rt * 16 + rbase + r;
     if (row >= a.rows) continue;
@@ -280,7 +296,9 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
 template <int HD>
 static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int NB = attn_chunk_blocks<HD>();
-  dim3 grid((a.rows + 63) / 64, a.splits, batch * a.n_kv_heads);
+  if (a.qblocks != (a.rows + 63) / 64 || a.n_eh != batch * a.n_kv_heads) return hipErrorInvalidValue;
+  const int groups = a.n_eh * a.splits;
+  dim3 grid(8 * ((groups + 7) / 8) * a.qblocks);
   hipEvent_t end_attn = a.splits == 1 ? ev1 : nullptr;
   const uint32_t lds = (uint32_t)(2 * NB * sizeof(AttnBlock<HD>));
   UAD_LAUNCH((attn_kernel<HD, NB>), grid, dim3(256), lds, s, ev0, end_attn, a);

@@ -34,11 +34,13 @@ __device__ __forceinline__ float gelu_tanh(float z) {
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
 constexpr int kMaxTilesPerGroup = 4;
+constexpr int kMaxSsqTiles = 2048 / 16;  // d_model <= 2048
 
 template <int EPI, int T, int KPW, bool DUAL>
 __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   extern __shared__ float red[];  // [waves][4*T*4 slots][64 lanes]
-  __shared__ float rpart[8][64];  // partial sums of ssq for rstd
+  constexpr bool kRstd = (EPI == EPI_QKV || EPI == EPI_GEGLU);
+  __shared__ float ssq_s[kRstd ? kMaxSsqTiles : 1][64];  // this group's rows' per-tile sums of squares
   __shared__ float rstd_s[64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -51,27 +53,6 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   const int KB = g.K / kTileK;
   const int passes = KB / (KPW * waves);
 
-  // rstd of this group's rows, from the residual GEMM's per-tile sums of
-  // squares (fixed summation order); loads issued before the operand loads
-  // (the first 16 tiles of each wave are unconditional loads with clamped
-  // indices so they issue back to back; d/16 tiles need more only when fewer
-  // than d/256 waves run)
-  if ((EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd) {
-    const int row = min(m0 + lane, g.M - 1);
-    float vals[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int j = wave + i * waves;
-      const float val = g.ssq[(size_t)min(j, g.ssq_tiles - 1) * g.m_alloc + row];
-      vals[i] = j < g.ssq_tiles ? val : 0.f;
-    }
-    float acc = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) acc += vals[i];
-    for (int j = wave + 16 * waves; j < g.ssq_tiles; j += waves) acc += g.ssq[(size_t)j * g.m_alloc + row];
-    rpart[wave][lane] = acc;
-  }
-
   f32x4 acc[kMaxTilesPerGroup][T], acc2[kMaxTilesPerGroup][DUAL ? T : 1];
 #pragma unroll
   for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
@@ -81,9 +62,10 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
     for (int t = 0; t < (DUAL ? T : 1); ++t) acc2[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int pass = 0; pass < passes; ++pass) {
+  // Operand loads of one pass (a run of KPW k-blocks per wave) and its MFMAs.
+  f16x8 w[KPW][T], a[KPW][kMaxTilesPerGroup], a2[KPW][DUAL ? kMaxTilesPerGroup : 1];
+  auto load_pass = [&](int pass) {
     const int kb0 = (pass * waves + wave) * KPW;
-    f16x8 w[KPW][T], a[KPW][kMaxTilesPerGroup], a2[KPW][DUAL ? kMaxTilesPerGroup : 1];
     const op_t *wp = g.W + ((size_t)tile0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
     for (int j = 0; j < KPW; ++j)
@@ -102,6 +84,8 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
           a2[j][mt] = ok ? *(const f16x8 *)(ap2 + ((size_t)mt * KB + j) * kBlockElems) : f16x8{};
       }
     }
+  };
+  auto mma_pass = [&]() {
 #pragma unroll
     for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
       if (mt >= nmt) break;
@@ -115,15 +99,66 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
                 __builtin_amdgcn_mfma_f32_16x16x32_f16(a2[j][mt], w[j][t], acc2[mt][DUAL ? t : 0], 0, 0, 0);
         }
     }
+  };
+
+  // The first pass's operand loads go out first: any wait for the loads
+  // issued after them (norm statistics, epilogue operands) covers them too,
+  // so the kernel pays one memory round trip before its first MFMA.
+  load_pass(0);
+  // Every global load the kernel needs is issued before the first use so a
+  // launch costs one memory round trip:
+  //  * rstd of this group's rows comes from the residual GEMM's per-tile sums
+  //    of squares; they go straight to LDS (LDS-direct loads, 64 rows of one
+  //    tile per wave instruction), so they hold no registers and nothing waits
+  //    on them before the main loop is done;
+  //  * the residual epilogue's h, gain / modulation and gate values of this
+  //    thread's first kEpiPrefetch output elements.
+  if (kRstd && g.use_rstd) {
+    const int srow = min(m0 + lane, g.M - 1);
+    for (int j = wave; j < g.ssq_tiles; j += waves)
+      __builtin_amdgcn_global_load_lds((const void *)(g.ssq + (size_t)j * g.m_alloc + srow),
+                                       (__attribute__((address_space(3))) void *)&ssq_s[j][0], 4, 0, 0);
   }
+  const int n_out_all = (EPI == EPI_GEGLU) ? nmt * 256 * (T / 2) : nmt * 256 * T;
+  constexpr int kEpiPrefetch = 2;
+  float pre_h[kEpiPrefetch], pre_s[kEpiPrefetch], pre_g[kEpiPrefetch];
+  if (EPI == EPI_RESID_F32) {
+    // branch-free: every load is unconditional from a valid address (h itself
+    // stands in for an absent operand) and the value is selected afterwards
+    const bool has_mod = g.mod_scale_next != nullptr, has_gain = g.gain_next != nullptr;
+    const bool has_gate = g.mod_gate != nullptr;
+#pragma unroll
+    for (int it = 0; it < kEpiPrefetch; ++it) {
+      const int e = it * (int)blockDim.x + threadIdx.x;
+      const int ln = e & 63, slot = e >> 6;
+      const int r = slot & 3, t = (slot >> 2) % T, mt = min((slot >> 2) / T, kMaxTilesPerGroup - 1);
+      const int row = min(m0 + mt * 16 + (ln >> 4) * 4 + r, g.M - 1);
+      const int col = min((tile0 + t) * 16 + (ln & 15), g.N - 1);
+      const float *hp = (const float *)g.out + (size_t)row * g.ldo + col;
+      const size_t ro = (size_t)row * g.mod_ld + col;
+      const float *sp = has_mod ? g.mod_scale_next + ro : (has_gain ? g.gain_next + col : hp);
+      const float *gp = has_gate ? g.mod_gate + ro : hp;
+      const float hv = *hp, sv = *sp, gv = *gp;
+      pre_h[it] = hv;
+      pre_s[it] = has_mod ? 1.0f + sv : (has_gain ? sv : 0.f);
+      pre_g[it] = has_gate ? gv : 1.0f;
+    }
+  }
+
+  for (int pass = 0; pass < passes; ++pass) {
+    if (pass > 0) load_pass(pass);
+    mma_pass();
+  }
+
+  if (kRstd && g.use_rstd) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the LDS-direct sums landed
 
   // Dual operand (normalised input = rstd * A + A2): fold rstd into each
   // wave's partial tile before the cross-wave reduction (it is linear).
   if (DUAL) {
-    __syncthreads();  // rpart complete
+    __syncthreads();  // ssq_s complete
     if (threadIdx.x < 64) {
       float ss = 0.f;
-      for (int w2 = 0; w2 < waves; ++w2) ss += rpart[w2][threadIdx.x];
+      for (int j = 0; j < g.ssq_tiles; ++j) ss += ssq_s[j][threadIdx.x];
       rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
     }
     __syncthreads();
@@ -146,9 +181,9 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[((wave * SLOTS) + (mt * T + t) * 4 + r) * 64 + lane] = acc[mt][t][r];
   __syncthreads();
-  if (!DUAL && (EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd && threadIdx.x < 64) {
+  if (!DUAL && kRstd && g.use_rstd && threadIdx.x < 64) {
     float ss = 0.f;
-    for (int w2 = 0; w2 < waves; ++w2) ss += rpart[w2][threadIdx.x];
+    for (int j = 0; j < g.ssq_tiles; ++j) ss += ssq_s[j][threadIdx.x];
     rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
   }
   __syncthreads();
@@ -157,8 +192,8 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   // GeGLU slot = (mt*(T/2) + pair)*4 + r); the D fragment of a 16x16 MFMA holds
   // row 4*(lane>>4)+r, column lane&15.  The per-wave trip count is uniform and
   // the 16 lanes holding one row are always active together.
-  const int n_out = (EPI == EPI_GEGLU) ? nmt * 256 * (T / 2) : nmt * 256 * T;
-  for (int e0 = 0; e0 < n_out; e0 += blockDim.x) {
+  const int n_out = n_out_all;
+  for (int e0 = 0, it = 0; e0 < n_out; e0 += blockDim.x, ++it) {
     const int e = e0 + threadIdx.x;
     if (e >= n_out) continue;  // whole waves only (n_out and blockDim are multiples of 64)
     const int ln = e & 63;
@@ -205,10 +240,20 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
     if (EPI == EPI_RESID_F32) {
       const int col = (tile0 + t) * 16 + (ln & 15);
       float hv = 0.f;
+      const bool pf = it < kEpiPrefetch;
+      float hv0 = 0.f, sc = 0.f, gt = 1.f;
+#pragma unroll
+      for (int k = 0; k < kEpiPrefetch; ++k)
+        if (it == k) { hv0 = pre_h[k]; sc = pre_s[k]; gt = pre_g[k]; }
       if (row_ok) {
         float *hp = (float *)g.out + (size_t)row * g.ldo + col;
-        const float gv = g.mod_gate ? g.mod_gate[(size_t)row * g.mod_ld + col] * v : v;
-        hv = (g.bias ? g.bias[col] : *hp) + gv;
+        const size_t ro = (size_t)row * g.mod_ld + col;
+        if (!pf) {
+          hv0 = g.bias ? 0.f : *hp;
+          sc = g.mod_scale_next ? 1.0f + g.mod_scale_next[ro] : (g.gain_next ? g.gain_next[col] : 0.f);
+          gt = g.mod_gate ? g.mod_gate[ro] : 1.0f;
+        }
+        hv = (g.bias ? g.bias[col] : hv0) + gt * v;
         *hp = hv;
       }
       float sq = hv * hv;  // sum over the 16 columns of this row (lanes sharing ln>>4)
@@ -216,11 +261,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
       if (row_ok) {
         if ((ln & 15) == 0) g.ssq[(size_t)(tile0 + t) * g.m_alloc + row] = sq;
-        if (g.mod_scale_next)
-          store_op(g.next + afrag_index(row, col, g.N / kTileK),
-                   hv * (1.0f + g.mod_scale_next[(size_t)row * g.mod_ld + col]));
-        else if (g.gain_next)
-          store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * g.gain_next[col]);
+        if (g.mod_scale_next || g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * sc);
       }
       continue;
     }

@@ -289,7 +289,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   // ssq holds the per-16-column sums of squares of h (RMSNorm folded into the GEMMs)
   size_t o_h = a.take<float>(M * d), o_te = a.take<uint16_t>(M * 2 * d), o_z = a.take<uint16_t>(M * d),
          o_n = a.take<uint16_t>(M * d), o_o = a.take<uint16_t>(M * c->q_dim), o_g = a.take<uint16_t>(M * F),
-         o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<float>(std::max<size_t>(part, 1) * c->hd),
+         o_q = a.take<uint16_t>(M * c->q_dim), o_op = a.take<uint16_t>(std::max<size_t>(part, 1) * c->hd),
          o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M),
          o_trx0 = a.take<float>(M * Da), o_trv = a.take<float>(M * Da), o_trt = a.take<float>(kMaxTrSteps * M),
          o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M),
@@ -308,7 +308,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->a_o = (op_t *)(ab + o_o);
   c->a_g = (op_t *)(ab + o_g);
   c->q = (__bf16 *)(ab + o_q);
-  c->attn_opart = (float *)(ab + o_op);
+  c->attn_opart = (op_t *)(ab + o_op);
   c->attn_ml = (float *)(ab + o_ml);
   c->ssq = (float *)(ab + o_ssq);
   c->tr_x0 = (float *)(ab + o_trx0);
@@ -662,6 +662,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     at.chunk = H; at.n_heads = c->Hq; at.n_kv_heads = c->Hkv; at.group = c->Hq / c->Hkv;
     at.rows = at.group * H; at.rows_pad = (at.rows + 63) / 64 * 64;
     at.splits = attn_splits(c, B, H, c->prefix_len, &at.blocks_per_split);
+    at.qblocks = (at.rows + 63) / 64; at.n_eh = B * c->Hkv;
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
     at.o = c->a_o; at.ldo = c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
 

@@ -137,11 +137,12 @@ struct AttnArgs {
   int n_keys;        // prefix + chunk
   int chunk, n_heads, n_kv_heads, group, rows, rows_pad;
   int splits, blocks_per_split;
+  int qblocks, n_eh;  // 64-row query blocks per environment-head; environment-heads (B * Hkv)
   float scale_log2;  // log2(e) / sqrt(hd)
   op_t *o;           // O-projection operand, fragment order, K = ldo
   int ldo;
-  float *opart;      // [splits][B*Hkv][rows_pad][hd] (splits > 1)
-  float *mlpart;     // [splits][B*Hkv][rows_pad][2]
+  op_t *opart;       // split partials o_s / l_s, fp16 (splits > 1), accumulator layout
+  float *mlpart;     // [splits][B*Hkv][rows_pad][2] (max, sum) per row
 };
 
 struct FinalArgs {
@@ -281,7 +282,8 @@ struct uad_ctx {
   float *h = nullptr;
   uad::op_t *a_te = nullptr, *a_z = nullptr, *a_n = nullptr, *a_o = nullptr, *a_g = nullptr;
   __bf16 *q = nullptr;
-  float *attn_opart = nullptr, *attn_ml = nullptr;
+  uad::op_t *attn_opart = nullptr;
+  float *attn_ml = nullptr;
   size_t attn_part_elems = 0;
   float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]
   void *abuf = nullptr;
