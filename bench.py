@@ -88,6 +88,93 @@ def step_flops(wl):
     return 2 * M * W.weight_param_count(s) + att
 
 
+def kernel_source_hash() -> str:
+    """sha256 over the library's kernel and host sources (byte counters are valid for exactly these)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_37772_amd", "csrc", "*"))):
+        if f.endswith((".hip", ".cpp", ".h")):
+            h.update(os.path.basename(f).encode())
+            with open(f, "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pi0_b1_traffic.json")
+
+
+def summarize_counters(run_dir: str) -> dict:
+    """Per-launch HBM traffic of every kernel class from two rocprofv3 --pmc runs of
+    ``bench.py --copy-calibration 256`` (FETCH_SIZE and WRITE_SIZE, KiB per dispatch),
+    each scaled so that the same counter reads 256 MiB for the plain 256 MiB copy."""
+    import csv
+    import statistics
+    out = {"source_hash": kernel_source_hash(), "unit": "bytes per launch", "classes": {}}
+    scale = {}
+    per_class = {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        rows = list(csv.DictReader(open(os.path.join(run_dir, f"pmc_{counter}", "run_counter_collection.csv"))))
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copies = [float(r["Counter_Value"]) for r in rows
+                  if "copyBuffer" in r["Kernel_Name"] and float(r["Counter_Value"]) > 100000]
+        scale[counter] = 256 * 1024 / statistics.mean(copies[-3:])
+        # walk the dispatches of every step and name each by its launch site
+        prev = None
+        for r in rows:
+            k = r["Kernel_Name"]
+            if "stamp_kernel" in k or "uad::" not in k:
+                continue
+            if "temb" in k:
+                cls = "temb"
+            elif "gemm_kernel<0," in k:
+                cls = "gemm_time_in"
+            elif "gemm_kernel<5," in k:
+                cls = "gemm_mod"
+            elif "gemm_kernel<4," in k:
+                cls = "gemm_qkv"
+            elif "attn_kernel" in k or "attn_combine" in k:
+                cls = "attention"
+            elif "gemm_kernel<3," in k:
+                cls = "gemm_gateup"
+            elif "gemm_kernel<1," in k:
+                cls = {"gemm_time_in": "gemm_time_out", "attention": "gemm_o", "gemm_gateup": "gemm_down"}.get(prev)
+            elif "final_kernel" in k:
+                cls = "final_euler"
+            else:
+                cls = None
+            if cls is None:
+                prev = None
+                continue
+            v = float(r["Counter_Value"]) * 1024 * scale[counter]
+            d = per_class.setdefault(cls, {}).setdefault(counter, [])
+            if cls == "attention" and prev == "attention" and "attn_combine" in k:
+                d[-1] += v  # the combine belongs to the same attention launch
+            else:
+                d.append(v)
+            prev = cls
+    for cls, d in per_class.items():
+        rd, wr = d.get("FETCH_SIZE", [0.0]), d.get("WRITE_SIZE", [0.0])
+        out["classes"][cls] = {"read": round(statistics.mean(rd)), "written": round(statistics.mean(wr)),
+                               "total": round(statistics.mean(rd) + statistics.mean(wr)), "launches": len(rd)}
+    out["calibration"] = {"copy_bytes": 256 << 20, "FETCH_SIZE_scale": round(scale["FETCH_SIZE"], 4),
+                          "WRITE_SIZE_scale": round(scale["WRITE_SIZE"], 4)}
+    return out
+
+
+def measured_traffic(kernel_class: str):
+    """Counter-measured bytes per launch of a class, if taken on the current sources; else None."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    c = t.get("classes", {}).get(kernel_class)
+    return c["total"] if c else None
+
+
 def cpu_baseline(wl, weights, prefix, noise, budgets, seconds, limit_threads=None):
     """Time the oracle (as it stands) on this host for a bounded sample of joint steps
     (BLAS threads capped at ``limit_threads`` when given)."""
@@ -136,10 +223,16 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-aal", action="store_true")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="print the per-launch traffic summary of two rocprofv3 --pmc runs found in DIR "
+                         "(pmc_FETCH_SIZE/, pmc_WRITE_SIZE/) and exit; no GPU needed")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy an MIB-MiB fp32 buffer 3 times (a plain copy kernel of known "
                          "size, the reference for hardware byte counters)")
     a = ap.parse_args()
+    if a.summarize_counters:
+        print(json.dumps(summarize_counters(a.summarize_counters), indent=1))
+        return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the hot path is measured on one "
                                    "MI355X and multi-GPU runs are not part of it", "n_gpus": a.gpus}))
@@ -245,11 +338,11 @@ def main():
     if batched:
         ach = kf[dom] / (dom_us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4), "traffic": None}
+                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4), "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None}
     else:
         ach = kb[dom] / (dom_us * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None}
     roof.update({"kernel": dom, "algorithmic_bytes_per_launch": kb[dom], "avg_launch_us": dom_us})
     sb = step_bytes(wl)
     step_roof = {"bytes_per_step": sb, "achieved_gbs": round(sb / (ms_step * 1e-3) / 1e9, 1),
