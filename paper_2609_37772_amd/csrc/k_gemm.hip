@@ -316,10 +316,8 @@ static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, 
 }
 
 // Launch shape.  Row groups: up to four 16-row tiles each; when the rows fit
-// in four tiles they are spread over more groups until the grid has about 256
-// workgroups (a last tile with fewer than 8 valid rows stays with the previous
-// group).  K: runs of KPW = 4 k-blocks per wave, <= 8 waves, as many passes as
-// needed.
+// in four tiles they are spread over more groups (see below).  K: runs of
+// KPW = 4 k-blocks per wave, <= 8 waves, as many passes as needed.
 GemmPlan plan_gemm(int epi, int M, int N, int K) {
   GemmPlan p{};
   const int KB = K / kTileK;
@@ -329,10 +327,12 @@ GemmPlan plan_gemm(int epi, int M, int N, int K) {
   if (MT > kMaxTilesPerGroup) {
     p.mgroups = (MT + kMaxTilesPerGroup - 1) / kMaxTilesPerGroup;
   } else {
-    int mt_eff = MT;
-    if (MT > 1 && M - (MT - 1) * 16 < 8) mt_eff = MT - 1;
-    int want = (256 + ngroups - 1) / ngroups;
-    p.mgroups = want < mt_eff ? want : mt_eff;
+    // small M: spread the row tiles over up to ~1.5 workgroups per CU (each
+    // extra group re-reads the weight tile from L2 but halves the activation
+    // rows per workgroup; measured best at batch 1: O and down 4 groups,
+    // QKV 2-3, gate/up 1)
+    const int want = 384 / ngroups;
+    p.mgroups = want < MT ? want : MT;
     if (p.mgroups < 1) p.mgroups = 1;
   }
   p.kpw = (KB % 4 == 0) ? 4 : (KB % 2 == 0 ? 2 : 1);
