@@ -234,7 +234,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int r = 0; r < 4; ++r) inv[r] = 1.0f / lr[r];
 #pragma unroll
     for (int nt = 0; nt < NTO; ++nt) {
-      typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
       *(f16x4 *)(op + nt * 256) = f16x4{(op_t)(o[nt][0] * inv[0]), (op_t)(o[nt][1] * inv[1]),
                                          (op_t)(o[nt][2] * inv[2]), (op_t)(o[nt][3] * inv[3])};
     }
@@ -259,7 +258,6 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
   const int ntiles = a.rows_pad / 16;
   const int lane = threadIdx.x;
   const int rbase = (lane >> 4) * 4;
-  typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
   f16x4 os[SMAX];
   float2 ml[SMAX][4];
 #pragma unroll

@@ -319,6 +319,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->mod = (float *)(ab + o_mod);
   c->mod_shift_ops = (op_t *)(ab + o_mshift);
   e = attention_init();
+  if (e == hipSuccess) e = gemm_init();
   if (e != hipSuccess) {
     uad_destroy(c);
     return cerr(UAD_E_HIP, std::string("attention kernel set-up: ") + hipGetErrorString(e));
@@ -629,7 +630,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, s,
                                         ea_, eb_));
       GemmArgs g{};
-      g.M = M;
+      g.M = M; g.m_alloc = (int)MA;
       g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = 2 * d;
       g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
       UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, 2 * d), s, ea_, eb_));
@@ -645,13 +646,15 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       UAD_CHECK_CLS(K_TEMB, launch_temb_ada(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
                                             c->h, c->ssq, (int)MA, s, ea_, eb_));
       GemmArgs g{};
-      g.M = M; g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = d; g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
+      g.M = M; g.m_alloc = (int)MA; g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = d; g.out = c->a_z; g.ldo = d;
+      g.bias = c->t1_b;
       UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, d), s, ea_, eb_));
       GemmArgs g2{};
-      g2.M = M; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d; g2.out = c->a_te; g2.ldo = d; g2.bias = c->t2_b;
+      g2.M = M; g2.m_alloc = (int)MA; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d; g2.out = c->a_te;
+      g2.ldo = d; g2.bias = c->t2_b;
       UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_SILU, g2, plan_gemm(EPI_BIAS_SILU, M, d, d), s, ea_, eb_));
       GemmArgs gm{};
-      gm.M = M; gm.A = c->a_te; gm.W = c->w_mod; gm.N = n_mod; gm.K = d; gm.out = c->mod; gm.ldo = n_mod;
+      gm.M = M; gm.m_alloc = (int)MA; gm.A = c->a_te; gm.W = c->w_mod; gm.N = n_mod; gm.K = d; gm.out = c->mod; gm.ldo = n_mod;
       gm.bias = c->b_mod; gm.mod_shift_ops = c->mod_shift_ops; gm.shift_stride = MA * d; gm.h_in = c->h;
       gm.d_model = d; gm.n_layers = c->L; gm.next = c->a_n;
       UAD_CHECK_CLS(K_GEMM_MOD, launch_gemm(EPI_MOD, gm, plan_gemm(EPI_MOD, M, n_mod, d), s, ea_, eb_));

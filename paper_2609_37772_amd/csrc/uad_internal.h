@@ -31,6 +31,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
 
 // Projection operands (weights and activations) are fp16.  The model's
 // weights are bf16 values and fp16 holds every bf16 value of magnitude in
@@ -101,7 +102,8 @@ struct GemmArgs {
   // squares of h over its 16 columns) and the next operand fp16(h * gain_next);
   // a consuming GEMM scales its accumulator by rstd[row] from those sums.
   float *ssq;             // [d/16][m_alloc]
-  int ssq_tiles, m_alloc;
+  int ssq_tiles;
+  int m_alloc;            // rows allocated in every operand / output buffer (>= M, multiple of 16)
   float eps;
   const float *gain_next; // EPI_RESID_F32: gain of the following RMSNorm (nullptr: none)
   op_t *next;             // EPI_RESID_F32: next operand, fragment order (K = N)
@@ -196,6 +198,7 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
 hipError_t launch_attention(const AttnArgs &a, int batch, int head_dim, hipStream_t s, hipEvent_t ev0 = nullptr,
                             hipEvent_t ev1 = nullptr);
 hipError_t attention_init();             // once per context: raise the kernels' LDS limit
+hipError_t gemm_init();                  // once per context: raise the batched GEMM's LDS limit
 int attention_chunk_blocks(int head_dim);  // 32-key blocks loaded per round trip
 int attention_max_splits(int head_dim);    // split-KV partials the combine accepts
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
