@@ -51,7 +51,10 @@ constexpr int attn_chunk_blocks() {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int HD, int NB>
+// LOWREG: the K fragments of each 16-key half and the V fragments of each
+// half of the output columns are read just before their MFMAs (fewer live
+// registers: two waves per SIMD at HD = 256) instead of all up front.
+template <int HD, int NB, bool LOWREG>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char attn_smem[];
   AttnBlock<HD> *bufs = (AttnBlock<HD> *)attn_smem;  // [2][NB]
@@ -139,24 +142,38 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       const int k0 = (c0 + j) * 32;
       // S^T for two 16-key halves: s[h][r] = score(query lane&15, key k0+16h+4(lane>>4)+r).
       // All K and V fragments of the block are read up front.
-      bf16x8 kf[2][KS], vf[NTO];
+      f32x4 s[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+      bf16x8 vf[LOWREG ? 1 : NTO];
+      if constexpr (LOWREG) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int row = 16 * h + (lane & 15);
+        for (int h = 0; h < 2; ++h) {
+          const int row = 16 * h + (lane & 15);
+          bf16x8 kf1[KS];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            kf1[ks] = *(const bf16x8 *)&blk.k[row * HD + (((ks * 4 + (lane >> 4)) ^ (row & 7)) * 8)];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf1[ks], qf[ks], s[h], 0, 0, 0);
+        }
+      } else {
+        bf16x8 kf[2][KS];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = 16 * h + (lane & 15);
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            kf[h][ks] = *(const bf16x8 *)&blk.k[row * HD + (((ks * 4 + (lane >> 4)) ^ (row & 7)) * 8)];
+        }
+#pragma unroll
+        for (int nt = 0; nt < NTO; ++nt) {
+          const int c = nt * 16 + (lane & 15);
+          vf[nt] = *(const bf16x8 *)&blk.vt[c * 32 + (((lane >> 4) ^ ((c >> 1) & 3)) * 8)];
+        }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          kf[h][ks] = *(const bf16x8 *)&blk.k[row * HD + (((ks * 4 + (lane >> 4)) ^ (row & 7)) * 8)];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[h][ks], qf[ks], s[h], 0, 0, 0);
       }
-#pragma unroll
-      for (int nt = 0; nt < NTO; ++nt) {
-        const int c = nt * 16 + (lane & 15);
-        vf[nt] = *(const bf16x8 *)&blk.vt[c * 32 + (((lane >> 4) ^ ((c >> 1) & 3)) * 8)];
-      }
-      f32x4 s[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[h][ks], qf[ks], s[h], 0, 0, 0);
       float mloc = -INFINITY;
 #pragma unroll
       for (int h = 0; h < 2; ++h)
@@ -197,8 +214,24 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         }
       l_run += psum;
       // O += P V : B operand lane l = V[keys of pf][col 16nt + (l&15)]
+      if constexpr (LOWREG) {
+        constexpr int HALF = NTO / 2;
 #pragma unroll
-      for (int nt = 0; nt < NTO; ++nt) o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf[nt], o[nt], 0, 0, 0);
+        for (int hh = 0; hh < 2; ++hh) {
+          bf16x8 vf1[HALF];
+#pragma unroll
+          for (int q = 0; q < HALF; ++q) {
+            const int c = (hh * HALF + q) * 16 + (lane & 15);
+            vf1[q] = *(const bf16x8 *)&blk.vt[c * 32 + (((lane >> 4) ^ ((c >> 1) & 3)) * 8)];
+          }
+#pragma unroll
+          for (int q = 0; q < HALF; ++q)
+            o[hh * HALF + q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf1[q], o[hh * HALF + q], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int nt = 0; nt < NTO; ++nt) o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf[nt], o[nt], 0, 0, 0);
+      }
     }
   }
 
@@ -298,8 +331,16 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
   const int groups = a.n_eh * a.splits;
   dim3 grid(8 * ((groups + 7) / 8) * a.qblocks);
   hipEvent_t end_attn = a.splits == 1 ? ev1 : nullptr;
-  const uint32_t lds = (uint32_t)(2 * NB * sizeof(AttnBlock<HD>));
-  UAD_LAUNCH((attn_kernel<HD, NB>), grid, dim3(256), lds, s, ev0, end_attn, a);
+  // Long splits (batched steps, one split per query block): one 32-key block
+  // per stage and K/V fragments streamed in halves, so that two workgroups
+  // (8 waves) share a CU and hide each other's LDS reads and softmax; short
+  // splits (batch 1): NB blocks per stage, one memory round trip per split.
+  const bool streamed = a.blocks_per_split > 2 * NB;
+  const uint32_t lds = (uint32_t)(2 * (streamed ? 1 : NB) * sizeof(AttnBlock<HD>));
+  if (streamed)
+    UAD_LAUNCH((attn_kernel<HD, 1, true>), grid, dim3(256), lds, s, ev0, end_attn, a);
+  else
+    UAD_LAUNCH((attn_kernel<HD, NB, false>), grid, dim3(256), lds, s, ev0, end_attn, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   hipEvent_t none = nullptr;
@@ -320,8 +361,12 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
 template <int HD>
 static hipError_t init_hd() {
   constexpr int NB = attn_chunk_blocks<HD>();
-  return hipFuncSetAttribute((const void *)attn_kernel<HD, NB>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)(2 * NB * sizeof(AttnBlock<HD>)));
+  hipError_t e = hipFuncSetAttribute((const void *)attn_kernel<HD, NB, false>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)(2 * NB * sizeof(AttnBlock<HD>)));
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(2 * sizeof(AttnBlock<HD>)));
+  return e;
 }
 
 hipError_t attention_init() {
