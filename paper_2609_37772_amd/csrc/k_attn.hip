@@ -51,6 +51,34 @@ constexpr int attn_chunk_blocks() {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// Workgroup wg of pf.wgs reads its 4 KiB-aligned share of the prefetch ranges
+// (16 bytes per lane per load, 8 loads in flight per lane: measured best of
+// 4 / 8 / 16 at batch 1, where fewer ran past the attention workgroups and
+// more slowed their own loads); what it read is
+// folded into one word that is stored only on an impossible match, which
+// keeps the loads from being removed.
+__device__ __forceinline__ void prefetch_share(const Prefetch &pf, int wg, unsigned *sink) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const uint32_t total = pf.bytes[0] + pf.bytes[1];
+  const uint32_t per = ((total + pf.wgs - 1) / pf.wgs + 4095u) & ~4095u;
+  const uint32_t beg = (uint32_t)wg * per, end = min(beg + per, total);
+  const uint32_t stride = blockDim.x * 16;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (uint32_t off0 = beg + threadIdx.x * 16; off0 < end; off0 += 8 * stride) {
+    u32x4 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t off = min(off0 + i * stride, end - 16);
+      const char *src = off < pf.bytes[0] ? pf.p[0] + off : pf.p[1] + (off - pf.bytes[0]);
+      v[i] = *(const u32x4 *)src;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc ^= v[i];
+  }
+  const unsigned w = acc.x ^ acc.y ^ acc.z ^ acc.w;
+  if (w == 0x9e3779b9u && threadIdx.x == 0 && wg == 0) *sink = w;
+}
+
 // LOWREG: the K fragments of each 16-key half and the V fragments of each
 // half of the output columns are read just before their MFMAs (fewer live
 // registers: two waves per SIMD at HD = 256) instead of all up front.
@@ -62,6 +90,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int NTO = HD / 16;  // 16-column output tiles
   constexpr int CPR = HD / 8;   // 16-byte chunks per K row
   constexpr int INS = HD / 64;  // LDS-direct instructions per wave per tile (4 waves x 64 lanes x 16 B)
+  if ((int)blockIdx.x >= (int)gridDim.x - a.pre_attn.wgs) {  // prefetch workgroups follow the attention ones
+    prefetch_share(a.pre_attn, blockIdx.x - (gridDim.x - a.pre_attn.wgs), a.pf_sink);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   // XCD-aware placement: the query blocks of one (environment-head, split)
@@ -285,8 +317,12 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
   const int rt = blockIdx.x;  // 16-row tile
   const int nt = blockIdx.y;  // 16-column tile
   const int eh = blockIdx.z;
+  const int n_eh = a.n_eh;
+  if (eh >= n_eh) {  // the extra slice prefetches
+    prefetch_share(a.pre_comb, blockIdx.y * gridDim.x + blockIdx.x, a.pf_sink);
+    return;
+  }
   const int b = eh / a.n_kv_heads, g = eh - b * a.n_kv_heads;
-  const int n_eh = gridDim.z;
   const int splits = a.splits;
   const int ntiles = a.rows_pad / 16;
   const int lane = threadIdx.x;
@@ -329,7 +365,9 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
   constexpr int NB = attn_chunk_blocks<HD>();
   if (a.qblocks != (a.rows + 63) / 64 || a.n_eh != batch * a.n_kv_heads) return hipErrorInvalidValue;
   const int groups = a.n_eh * a.splits;
-  dim3 grid(8 * ((groups + 7) / 8) * a.qblocks);
+  if (a.pre_attn.wgs < 0 || a.pre_comb.wgs < 0 || ((a.pre_attn.wgs || a.pre_comb.wgs) && !a.pf_sink))
+    return hipErrorInvalidValue;
+  dim3 grid(8 * ((groups + 7) / 8) * a.qblocks + a.pre_attn.wgs);
   hipEvent_t end_attn = a.splits == 1 ? ev1 : nullptr;
   // Long splits (batched steps, one split per query block): one 32-key block
   // per stage and K/V fragments streamed in halves, so that two workgroups
@@ -344,15 +382,17 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   hipEvent_t none = nullptr;
-  const dim3 cgrid(a.rows_pad / 16, HD / 16, batch * a.n_kv_heads);
+  AttnArgs ac = a;
+  ac.pre_comb.wgs = a.pre_comb.wgs ? (a.rows_pad / 16) * (HD / 16) : 0;  // one extra z slice
+  const dim3 cgrid(a.rows_pad / 16, HD / 16, batch * a.n_kv_heads + (ac.pre_comb.wgs ? 1 : 0));
   if (a.splits <= 4)
-    UAD_LAUNCH((attn_combine_kernel<4>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+    UAD_LAUNCH((attn_combine_kernel<4>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
   else if (a.splits <= 8)
-    UAD_LAUNCH((attn_combine_kernel<8>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+    UAD_LAUNCH((attn_combine_kernel<8>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
   else if (a.splits <= 16)
-    UAD_LAUNCH((attn_combine_kernel<16>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+    UAD_LAUNCH((attn_combine_kernel<16>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
   else if (a.splits <= 32)
-    UAD_LAUNCH((attn_combine_kernel<32>), cgrid, dim3(64), 0, s, none, ev1, a, HD);
+    UAD_LAUNCH((attn_combine_kernel<32>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

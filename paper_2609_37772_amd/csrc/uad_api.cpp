@@ -172,6 +172,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   uad_ctx *c = new uad_ctx();
   c->cfg = m;
   c->device = device;
+  e = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device);
+  if (e != hipSuccess) return cerr(UAD_E_HIP, std::string("hipDeviceGetAttribute: ") + hipGetErrorString(e));
   c->d = m.d_model;
   c->L = m.n_layers;
   c->Hq = m.n_heads;
@@ -293,7 +295,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
          o_ml = a.take<float>(std::max<size_t>(part, 1) * 2), o_ssq = a.take<float>((size_t)(d / 16) * M),
          o_trx0 = a.take<float>(M * Da), o_trv = a.take<float>(M * Da), o_trt = a.take<float>(kMaxTrSteps * M),
          o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M),
-         o_mod = a.take<float>(M * c->n_mod), o_mshift = a.take<uint16_t>(c->ada ? (size_t)2 * c->L * M * d : 0);
+         o_mod = a.take<float>(M * c->n_mod), o_mshift = a.take<uint16_t>(c->ada ? (size_t)2 * c->L * M * d : 0),
+         o_pf = a.take<unsigned>(64);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -318,6 +321,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->tr_mask = (uint8_t *)(ab + o_trm);
   c->mod = (float *)(ab + o_mod);
   c->mod_shift_ops = (op_t *)(ab + o_mshift);
+  c->pf_sink = (unsigned *)(ab + o_pf);
   e = attention_init();
   if (e == hipSuccess) e = gemm_init();
   if (e != hipSuccess) {
@@ -668,6 +672,14 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     at.qblocks = (at.rows + 63) / 64; at.n_eh = B * c->Hkv;
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
     at.o = c->a_o; at.ldo = c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
+    at.pf_sink = c->pf_sink;
+    // Weight prefetch on otherwise idle CUs: when the attention leaves CUs free
+    // (batch 1), its extra workgroups read the layer's O and gate/up weights and
+    // the split merge's extra slice reads the down weights and the next
+    // layer's QKV weights, so those projections stream them from the
+    // memory-side cache instead of HBM.
+    const int attn_wgs = 8 * ((at.n_eh * at.splits + 7) / 8) * at.qblocks;
+    const int spare_cus = c->n_cu - attn_wgs;
 
     const GemmPlan pq = plan_gemm(EPI_QKV, M, c->n_qkv, d);
     const GemmPlan po = plan_gemm(EPI_RESID_F32, M, d, c->q_dim);
@@ -685,6 +697,22 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       if (c->ada) q.A2 = c->mod_shift_ops + (size_t)(2 * l) * MA * d;
       UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, pq, s, ea_, eb_));
       at.kc = kc; at.vtc = vtc;
+      at.pre_attn = Prefetch{};
+      at.pre_comb = Prefetch{};
+      if (spare_cus >= 32) {
+        at.pre_attn.p[0] = (const char *)lp.wo;
+        at.pre_attn.bytes[0] = (uint32_t)((size_t)d * c->q_dim * sizeof(op_t));
+        at.pre_attn.p[1] = (const char *)lp.wgu;
+        at.pre_attn.bytes[1] = (uint32_t)((size_t)2 * F * d * sizeof(op_t));
+        at.pre_attn.wgs = spare_cus;
+        if (at.splits > 1) {
+          at.pre_comb.p[0] = (const char *)lp.wdown;
+          at.pre_comb.bytes[0] = (uint32_t)((size_t)d * F * sizeof(op_t));
+          at.pre_comb.p[1] = (const char *)c->layers[(l + 1) % c->L].wqkv;
+          at.pre_comb.bytes[1] = (uint32_t)((size_t)c->n_qkv * d * sizeof(op_t));
+          at.pre_comb.wgs = 1;
+        }
+      }
       UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s, ea_, eb_));
       GemmArgs o{};
       o.M = M; o.A = c->a_o; o.W = lp.wo; o.N = d; o.K = c->q_dim;

@@ -130,6 +130,15 @@ struct GemmArgs {
   int chunk, prefix, s_alloc, n_kv_heads, head_dim, q_dim;
 };
 
+// Up to two byte ranges (weights of the next projections) that otherwise idle
+// workgroups of a latency-bound launch read ahead of their use, so that the
+// projections find them in the memory-side cache instead of HBM.
+struct Prefetch {
+  const char *p[2];
+  uint32_t bytes[2];  // multiples of 16
+  int wgs;            // workgroups given to it (0: no prefetch)
+};
+
 struct AttnArgs {
   const __bf16 *q;  // [M][ldq] bf16, query head j at columns j*hd
   int ldq;
@@ -145,6 +154,9 @@ struct AttnArgs {
   int ldo;
   op_t *opart;       // split partials o_s / l_s, fp16 (splits > 1), accumulator layout
   float *mlpart;     // [splits][B*Hkv][rows_pad][2] (max, sum) per row
+  Prefetch pre_attn;  // read by extra workgroups of the attention kernel
+  Prefetch pre_comb;  // read by an extra slice of the split-merge grid (wgs: nonzero = on)
+  unsigned *pf_sink;  // one word the prefetch may write (keeps its loads alive)
 };
 
 struct FinalArgs {
@@ -287,6 +299,8 @@ struct uad_ctx {
   __bf16 *q = nullptr;
   uad::op_t *attn_opart = nullptr;
   float *attn_ml = nullptr;
+  unsigned *pf_sink = nullptr;
+  int n_cu = 0;  // compute units of the device
   size_t attn_part_elems = 0;
   float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]
   void *abuf = nullptr;
