@@ -27,14 +27,21 @@
 namespace uad {
 
 // tanh-approximate GELU, 0.5 z (1 + tanh(u)) with u = sqrt(2/pi) (z + 0.044715 z^3),
-// evaluated as z * sigmoid(2u) = z / (1 + e^{-2u}) (the same function; one
-// exponential instead of a tanh)
+// evaluated as z * sigmoid(2u) = z / (1 + 2^(-2u log2 e)) (the same function)
+// with the hardware exp2 and reciprocal (~1 ulp each; the results are stored
+// as fp16): an IEEE division here made the gate/up epilogue ALU-bound.  Large
+// negative z gives -0 (2^t -> inf), large positive z gives z, NaN propagates.
 __device__ __forceinline__ float gelu_tanh(float z) {
-  const float two_c = 1.5957691216057308f;  // 2 sqrt(2/pi)
-  return z / (1.0f + __expf(-two_c * (z + 0.044715f * z * z * z)));
+  const float k1 = -2.3022081983f;    // -2 sqrt(2/pi) log2(e)
+  const float k2 = -0.1029432396f;    // k1 * 0.044715
+  const float t = z * __builtin_fmaf(k2, z * z, k1);
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
 }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+// SiLU z * sigmoid(z), by the same exp2 / reciprocal route
+__device__ __forceinline__ float silu(float z) {
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950409f * z));
+}
 
 // Epilogue of one output element (row, col = 16 * tile + (ln & 15)) given its
 // accumulated value v (and, for GeGLU, the matching up-projection value u);
