@@ -93,3 +93,36 @@ def test_adarms_time_changes_velocity(gpu):
                       torch.zeros((1, H), dtype=torch.uint8, device="cuda"), vg)
         vs.append(vg.cpu().numpy())
     assert np.abs(vs[0] - vs[1]).max() > 1e-3
+
+
+def test_adarms_batched_sampled_envs(gpu):
+    """8 environments, M = 400 rows: the batched projection kernel serves the
+    time MLP, the modulation GEMM and the gated residual epilogues.  Sampled
+    environments against the oracle run alone: one teacher-forced step, then
+    the free-running UAD schedule."""
+    c = case("pi05_b1_adarms", batch=8)
+    B, H = c.budgets.shape
+    bud = np.full((B, H), 10, np.int32)
+    bud[:, : H // 10] = 4
+    bud[:, H // 10: H // 2] = 7
+    n, t, dt, mask = O.build_schedule(bud)
+    xg = dev(c.noise.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)), dev(mask[0].astype(np.uint8)), vg)
+    torch.cuda.synchronize()
+    v = vg.cpu().numpy()
+    nt, tg, dtg, mg = c.expert.schedule_tables(bud)
+    x = dev(c.noise.astype(np.float32))
+    rel = torch.zeros_like(x)
+    rst = torch.full(bud.shape, -1, dtype=torch.int32, device="cuda")
+    c.expert.schedule(x, tg, dtg, mg, rel, rst)
+    torch.cuda.synchronize()
+    rel = rel.cpu().numpy()
+    for b in (0, B - 1):
+        mb = c.oracle_model([b])
+        e = rel_err(v[b], O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0])
+        r = O.denoise_schedule(mb, c.noise[b:b + 1], bud[b:b + 1])
+        ea = float(np.abs(rel[b] - r["released"][0]).max())
+        log(f"[pi05 B=8] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
+        assert e <= VEL_RTOL and ea <= ACT_ATOL
+    np.testing.assert_array_equal(rst.cpu().numpy(), O.release_steps(bud))
