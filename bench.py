@@ -344,6 +344,14 @@ def main():
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None}
     roof.update({"kernel": dom, "algorithmic_bytes_per_launch": kb[dom], "avg_launch_us": dom_us})
+    if dom == "attention" and not batched:
+        # at batch 1 the attention launches carry the read-ahead of the next
+        # projections' weights (O, gate/up, down, next layer's QKV) on the CUs they
+        # leave idle: part of their measured traffic, none of their algorithmic bytes
+        s = wl.shape
+        d, F, qd = s.d_model, s.d_ff, s.n_heads * s.head_dim
+        nqkv = qd + 2 * s.n_kv_heads * s.head_dim
+        roof["prefetch_bytes_per_launch"] = 2 * (d * qd + 2 * F * d + d * F + nqkv * d)
     sb = step_bytes(wl)
     step_roof = {"bytes_per_step": sb, "achieved_gbs": round(sb / (ms_step * 1e-3) / 1e9, 1),
                  "hbm_frac": round(sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
