@@ -175,6 +175,39 @@ def measured_traffic(kernel_class: str):
     return c["total"] if c else None
 
 
+def streaming_copy_gbs(torch, mib=2048, reps=10):
+    """Measured HBM streaming rate of this device: a plain device-to-device copy
+    of `mib` MiB (bytes read + bytes written per second), after the timed region."""
+    src = torch.empty(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    del src, dst
+    return 2 * (mib << 20) * reps / el / 1e9
+
+
+def cpu_model():
+    """The host CPU's model name (and the cores this process may run on)."""
+    name = platform.processor() or "host"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        return f"{name}, {len(os.sched_getaffinity(0))} cores available"
+    except AttributeError:
+        return name
+
+
 def cpu_baseline(wl, weights, prefix, noise, budgets, seconds, limit_threads=None):
     """Time the oracle (as it stands) on this host for a bounded sample of joint steps
     (BLAS threads capped at ``limit_threads`` when given)."""
@@ -210,7 +243,7 @@ def _cpu_baseline_run(wl, weights, prefix, noise, budgets, seconds, threads, O):
             break
     return {"value": done / el, "unit": "denoise steps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{done} joint steps of the {wl.name} workload (B={wl.batch}, H={wl.chunk}, "
-                      f"P={wl.prefix}) in {el:.1f} s, numpy fp32 BLAS on {platform.processor() or 'host'}",
+                      f"P={wl.prefix}) in {el:.1f} s, numpy fp32 BLAS on {cpu_model()}",
             "seconds": el}
 
 
@@ -220,6 +253,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="pi0_b1")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the workload's environment count (e.g. one GPU's share of a sharded fleet)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-aal", action="store_true")
@@ -247,7 +282,7 @@ def main():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(2)
     U.load_library()
-    wl = W.get_workload(a.workload)
+    wl = W.get_workload(a.workload, **({"batch": a.batch} if a.batch > 0 else {}))
     s = wl.shape
     B, H, P, M = wl.batch, wl.chunk, wl.prefix, wl.batch * wl.chunk
     log(f"[bench] workload {wl.name}: L={s.n_layers} d={s.d_model} B={B} H={H} P={P}")
@@ -296,7 +331,7 @@ def main():
     hz = ex.tick_rate_hz()
     ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
     per_sched = []
-    for _ in range(max(20, n_timed)):
+    for _ in range(max(100, n_timed)):
         x.copy_(x0)
         ex.schedule(x, tg, dtg, mg, None, None, ticks)
         torch.cuda.synchronize()
@@ -353,8 +388,11 @@ def main():
         nqkv = qd + 2 * s.n_kv_heads * s.head_dim
         roof["prefetch_bytes_per_launch"] = 2 * (d * qd + 2 * F * d + d * F + nqkv * d)
     sb = step_bytes(wl)
+    copy_gbs = streaming_copy_gbs(torch)
     step_roof = {"bytes_per_step": sb, "achieved_gbs": round(sb / (ms_step * 1e-3) / 1e9, 1),
                  "hbm_frac": round(sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "hbm_copy_gbs": round(copy_gbs, 1),
+                 "copy_frac": round(sb / (ms_step * 1e-3) / 1e9 / copy_gbs, 4),
                  "flops_per_step": step_flops(wl),
                  "mfma_frac": round(step_flops(wl) / (ms_step * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)}
     log(f"[bench] dominant kernel {dom}: {dom_us:.2f} us/launch, {roof['achieved']} {roof['unit']}")
