@@ -129,14 +129,20 @@ int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) {
   const int qblocks = (rows + 63) / 64;
   const int n_blocks = (P + H + 31) / 32;
   const int wgs = qblocks * B * c->Hkv;
-  int per = n_blocks;
-  if (wgs < 128) {
-    // small batch: split the keys so each split is one chunk (one memory round trip)
-    per = attention_chunk_blocks(c->hd);
-    const int smax = attention_max_splits(c->hd);
-    if ((n_blocks + per - 1) / per > smax) per = (n_blocks + smax - 1) / smax;
-    if (per > n_blocks) per = n_blocks;
+  // Split the keys so that the query blocks x splits fill about one round of
+  // workgroups (256 CUs): one chunk (one memory round trip) per split when
+  // that fits (batch 1), else floor(256 / query blocks) splits (a few
+  // environments; measured best at 4 and 8 environments), none when the query
+  // blocks alone fill the chip.
+  const int nb = attention_chunk_blocks(c->hd);
+  int per = nb;
+  if ((long)wgs * ((n_blocks + nb - 1) / nb) > 256) {
+    const int sp = std::max(1, 256 / wgs);
+    per = (n_blocks + sp - 1) / sp;
   }
+  const int smax = attention_max_splits(c->hd);
+  if ((n_blocks + per - 1) / per > smax) per = (n_blocks + smax - 1) / smax;
+  if (per > n_blocks) per = n_blocks;
   *bps = per;
   return (n_blocks + per - 1) / per;
 }
