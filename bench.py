@@ -258,6 +258,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-aal", action="store_true")
+    ap.add_argument("--sched-reps", type=int, default=100,
+                    help="schedules timed one by one for the median / bootstrap interval (fewer for profiler runs)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
                     help="print the per-launch traffic summary of two rocprofv3 --pmc runs found in DIR "
                          "(pmc_FETCH_SIZE/, pmc_WRITE_SIZE/) and exit; no GPU needed")
@@ -331,7 +333,7 @@ def main():
     hz = ex.tick_rate_hz()
     ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
     per_sched = []
-    for _ in range(max(100, n_timed)):
+    for _ in range(max(1, a.sched_reps)):
         x.copy_(x0)
         ex.schedule(x, tg, dtg, mg, None, None, ticks)
         torch.cuda.synchronize()
