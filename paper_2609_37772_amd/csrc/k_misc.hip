@@ -29,7 +29,10 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
   const int KB = 2 * d / kTileK;
   if (threadIdx.x < Da) xs[threadIdx.x] = x[(size_t)m * Da + threadIdx.x];
   __syncthreads();
-  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+  // workgroup (m, y) owns columns y * blockDim.x + tid of the action
+  // projection and the same indices of the sinusoids
+  const int n = blockIdx.y * blockDim.x + threadIdx.x;
+  if (n < d) {
     float acc = b_in[n];
     const float *w = w_in + (size_t)n * Da;
     for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
@@ -37,10 +40,10 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
   }
   const float tm = t[m];
   const int half = d >> 1;
-  for (int j = threadIdx.x; j < half; j += blockDim.x) {
-    const float arg = freqs[j] * tm;
-    store_op(te + afrag_index(m, d + j, KB), sinf(arg));
-    store_op(te + afrag_index(m, d + half + j, KB), cosf(arg));
+  if (n < half) {
+    const float arg = freqs[n] * tm;
+    store_op(te + afrag_index(m, d + n, KB), sinf(arg));
+    store_op(te + afrag_index(m, d + half + n, KB), cosf(arg));
   }
 }
 
@@ -58,8 +61,10 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
   const int KB = d / kTileK;
   if (threadIdx.x < Da) xs[threadIdx.x] = x[(size_t)m * Da + threadIdx.x];
   __syncthreads();
-  // d is a multiple of 32, so the 16 lanes of a 16-column tile are active together
-  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+  // workgroup (m, y) owns columns y * blockDim.x + tid; d is a multiple of
+  // 32, so the 16 lanes of a 16-column tile are active together
+  const int n = blockIdx.y * blockDim.x + threadIdx.x;
+  if (n < d) {
     float acc = b_in[n];
     const float *w = w_in + (size_t)n * Da;
     for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
@@ -71,10 +76,10 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
   }
   const float tm = t[m];
   const int half = d >> 1;
-  for (int j = threadIdx.x; j < half; j += blockDim.x) {
-    const float arg = freqs[j] * tm;
-    store_op(te + afrag_index(m, j, KB), sinf(arg));
-    store_op(te + afrag_index(m, half + j, KB), cosf(arg));
+  if (n < half) {
+    const float arg = freqs[n] * tm;
+    store_op(te + afrag_index(m, n, KB), sinf(arg));
+    store_op(te + afrag_index(m, half + n, KB), cosf(arg));
   }
 }
 
@@ -211,14 +216,14 @@ __global__ void stamp_kernel(uint64_t *dst) {
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                        const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
-  UAD_LAUNCH(temb_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te);
+  UAD_LAUNCH(temb_kernel, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te);
   return hipGetLastError();
 }
 
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                            const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
                            hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  UAD_LAUNCH(temb_ada_kernel, dim3(M), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, h, ssq,
+  UAD_LAUNCH(temb_ada_kernel, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, h, ssq,
              m_alloc);
   return hipGetLastError();
 }
