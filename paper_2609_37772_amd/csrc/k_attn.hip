@@ -184,6 +184,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
             kf1[ks] = *(const bf16x8 *)&blk.k[row * HD + (((ks * 4 + (lane >> 4)) ^ (row & 7)) * 8)];
+          __builtin_amdgcn_sched_barrier(0);  // all reads of the half issued before its MFMAs
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf1[ks], qf[ks], s[h], 0, 0, 0);
         }
@@ -256,6 +257,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             const int c = (hh * HALF + q) * 16 + (lane & 15);
             vf1[q] = *(const bf16x8 *)&blk.vt[c * 32 + (((lane >> 4) ^ ((c >> 1) & 3)) * 8)];
           }
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
           for (int q = 0; q < HALF; ++q)
             o[hh * HALF + q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf1[q], o[hh * HALF + q], 0, 0, 0);
