@@ -1,0 +1,120 @@
+"""GPU edge cases through the C ABI: argument errors of a step and a schedule
+(empty and oversized shapes, missing state), the shortest and longest
+schedules (every budget 1; a budget of 64, the largest the schedule builder
+takes), and a mid-size batch (8 environments, 400 rows) where the attention
+splits its keys over a few long streamed splits and the projections mix the
+small-M and the batched kernels.
+
+Bars as for the other parity tests: velocities within a normwise max
+relative error of 2e-2, released actions within 1e-2 absolute, release steps
+bit-exact.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2609_37772_amd as U
+from tests.harness import log, make_case, rel_err
+
+pytestmark = pytest.mark.gpu
+
+VEL_RTOL = 2e-2
+ACT_ATOL = 1e-2
+_cases = {}
+
+
+def case(name, **kw):
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cases:
+        _cases[key] = make_case(name, **kw)
+    return _cases[key]
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def schedule_gpu(c, budgets):
+    n, tg, dtg, mg = c.expert.schedule_tables(budgets)
+    x = dev(c.noise.astype(np.float32))
+    rel = torch.zeros_like(x)
+    rst = torch.full(budgets.shape, -1, dtype=torch.int32, device="cuda")
+    c.expert.schedule(x, tg, dtg, mg, rel, rst)
+    torch.cuda.synchronize()
+    return n, x.cpu().numpy(), rel.cpu().numpy(), rst.cpu().numpy()
+
+
+def test_step_and_schedule_argument_errors(gpu):
+    """Zero or oversized batch / chunk, null pointers, zero steps: rejected
+    before any device work, with the status the header documents."""
+    c = case("tiny")
+    lib = U.load_library()
+    B, H, Da = c.noise.shape
+    x = dev(c.noise.astype(np.float32))
+    t = torch.ones((B, H), device="cuda")
+    dt = torch.zeros((B, H), device="cuda")
+    m = torch.zeros((B, H), dtype=torch.uint8, device="cuda")
+    p = [ctypes.c_void_p(v.data_ptr()) for v in (x, t, dt, m)]
+    ctx = c.expert.ctx
+    for bb, hh, want in [(0, H, 1), (B, 0, 1), (-1, H, 1), (B + 1, H, 2), (B, H + 1000, 2)]:
+        assert lib.uad_denoise_step(ctx, *p, None, bb, hh) == want
+        assert lib.uad_denoise_schedule(ctx, *p, 1, bb, hh, None, None, None) == want
+    assert lib.uad_denoise_step(ctx, None, *p[1:], None, B, H) == 1
+    assert lib.uad_denoise_schedule(ctx, *p, 0, B, H, None, None, None) == 1
+    assert "n_steps" in U.uad_last_error(ctx)
+    # a context without weights or prefix: UAD_E_STATE
+    fresh = U.ActionExpert(c.wl.shape, B, H, c.wl.prefix)
+    try:
+        assert lib.uad_denoise_step(fresh.ctx, *p, None, B, H) == 3
+        assert "weights" in U.uad_last_error(fresh.ctx)
+    finally:
+        fresh.close()
+    # the valid call still works afterwards
+    c.expert.step(x, t, dt, m)
+    torch.cuda.synchronize()
+    assert torch.equal(x.cpu(), torch.from_numpy(c.noise.astype(np.float32)))  # dt = 0: unchanged
+
+
+@pytest.mark.parametrize("kind", ["all_ones", "max_budget"])
+def test_shortest_and_longest_schedules(gpu, kind):
+    c = case("tiny")
+    B, H = c.budgets.shape
+    if kind == "all_ones":
+        bud = np.ones((B, H), np.int32)
+    else:
+        bud = np.full((B, H), 10, np.int32)
+        bud[0, ::3] = 64
+        bud[0, 1] = 1
+    r = O.denoise_schedule(c.oracle_model(), c.noise, bud)
+    n, x, rel, rst = schedule_gpu(c, bud)
+    assert n == int(bud.max())
+    ex, er = float(np.abs(x - r["x"]).max()), float(np.abs(rel - r["released"]).max())
+    log(f"[tiny {kind}] {n} steps: final max abs err {ex:.2e}, released {er:.2e}")
+    assert ex <= ACT_ATOL and er <= ACT_ATOL
+    np.testing.assert_array_equal(rst, r["release_step"])
+
+
+def test_mid_batch_sampled_envs(gpu):
+    """8 environments of the pi0-scale model (400 rows): streamed split-KV
+    attention with a merge, mixed projection kernels; sampled environments
+    against the oracle run alone."""
+    c = case("pi0_fleet_b64", batch=8)
+    B, H = c.budgets.shape
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    xg = dev(c.noise.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)), dev(mask[0].astype(np.uint8)), vg)
+    torch.cuda.synchronize()
+    v = vg.cpu().numpy()
+    _, x, rel, rst = schedule_gpu(c, c.budgets)
+    for b in (0, B - 1):
+        mb = c.oracle_model([b])
+        e = rel_err(v[b], O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0])
+        r = O.denoise_schedule(mb, c.noise[b:b + 1], c.budgets[b:b + 1])
+        ea = float(np.abs(rel[b] - r["released"][0]).max())
+        log(f"[pi0 B=8] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
+        assert e <= VEL_RTOL and ea <= ACT_ATOL
+    np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
