@@ -17,70 +17,105 @@ __device__ __forceinline__ float block_sum_256(float v, float *scratch) {
   return (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
 }
 
+// Rows per workgroup of the embedding kernels: R tokens share one read of
+// their columns' W_in rows (R = 16 when batched: with one token per
+// workgroup the 3,200-token fleet re-read W_in 3,200 times from L2).
+template <int R>
+__device__ __forceinline__ int load_action_rows(const float *__restrict__ x, int M, int Da, float (*xs)[64]) {
+  const int m0 = blockIdx.x * R;
+  const int rows = min(R, M - m0);
+  for (int i = threadIdx.x; i < rows * Da; i += blockDim.x) {
+    const int r = i / Da, j = i - r * Da;
+    xs[r][j] = x[(size_t)(m0 + r) * Da + j];
+  }
+  __syncthreads();
+  return rows;
+}
+
 // te[m] = [ x_m W_in^T + b_in ; sin(w t_m) ; cos(w t_m) ] as the fp16 operand
 // of the time MLP in fragment order (K = 2d): the per-token flow-time
-// conditioning placed before the action MLP.
-__global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, const float *__restrict__ t,
+// conditioning placed before the action MLP.  Workgroup (g, y): tokens
+// g R .. g R + R - 1, columns y * blockDim.x + tid of the action projection
+// and the same indices of the sinusoids.
+template <int R>
+__global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, const float *__restrict__ t, int M,
                                                     int Da, int d, const float *__restrict__ w_in,
                                                     const float *__restrict__ b_in,
                                                     const float *__restrict__ freqs, op_t *__restrict__ te) {
-  __shared__ float xs[64];
-  const int m = blockIdx.x;
+  __shared__ float xs[R][64];
+  const int m0 = blockIdx.x * R;
+  const int rows = load_action_rows<R>(x, M, Da, xs);
   const int KB = 2 * d / kTileK;
-  if (threadIdx.x < Da) xs[threadIdx.x] = x[(size_t)m * Da + threadIdx.x];
-  __syncthreads();
-  // workgroup (m, y) owns columns y * blockDim.x + tid of the action
-  // projection and the same indices of the sinusoids
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
   if (n < d) {
-    float acc = b_in[n];
+    float acc[R];
+    const float bn = b_in[n];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = bn;
     const float *w = w_in + (size_t)n * Da;
-    for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
-    store_op(te + afrag_index(m, n, KB), acc);
+    for (int j = 0; j < Da; ++j) {
+      const float wj = w[j];
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] += xs[r][j] * wj;  // rows past the end: never stored
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (r < rows) store_op(te + afrag_index(m0 + r, n, KB), acc[r]);
   }
-  const float tm = t[m];
   const int half = d >> 1;
-  if (n < half) {
-    const float arg = freqs[n] * tm;
-    store_op(te + afrag_index(m, d + n, KB), sinf(arg));
-    store_op(te + afrag_index(m, d + half + n, KB), cosf(arg));
-  }
+  if (n < half)
+    for (int r = 0; r < rows; ++r) {
+      const float arg = freqs[n] * t[m0 + r];
+      store_op(te + afrag_index(m0 + r, d + n, KB), sinf(arg));
+      store_op(te + afrag_index(m0 + r, d + half + n, KB), cosf(arg));
+    }
 }
 
 // Adaptive-norm variant: te[m] = e(t_m) alone (K = d) as the time MLP's fp16
 // operand; the action token itself starts the residual stream,
 // h[m] = x_m W_in^T + b_in (fp32), with its per-16-column sums of squares.
+template <int R>
 __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__ x, const float *__restrict__ t,
-                                                        int Da, int d, const float *__restrict__ w_in,
+                                                        int M, int Da, int d, const float *__restrict__ w_in,
                                                         const float *__restrict__ b_in,
                                                         const float *__restrict__ freqs, op_t *__restrict__ te,
                                                         float *__restrict__ h, float *__restrict__ ssq,
                                                         int m_alloc) {
-  __shared__ float xs[64];
-  const int m = blockIdx.x;
+  __shared__ float xs[R][64];
+  const int m0 = blockIdx.x * R;
+  const int rows = load_action_rows<R>(x, M, Da, xs);
   const int KB = d / kTileK;
-  if (threadIdx.x < Da) xs[threadIdx.x] = x[(size_t)m * Da + threadIdx.x];
-  __syncthreads();
-  // workgroup (m, y) owns columns y * blockDim.x + tid; d is a multiple of
-  // 32, so the 16 lanes of a 16-column tile are active together
+  // d is a multiple of 32, so the 16 lanes of a 16-column tile are active together
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
   if (n < d) {
-    float acc = b_in[n];
-    const float *w = w_in + (size_t)n * Da;
-    for (int j = 0; j < Da; ++j) acc += xs[j] * w[j];
-    h[(size_t)m * d + n] = acc;
-    float sq = acc * acc;
+    float acc[R];
+    const float bn = b_in[n];
 #pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
-    if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
+    for (int r = 0; r < R; ++r) acc[r] = bn;
+    const float *w = w_in + (size_t)n * Da;
+    for (int j = 0; j < Da; ++j) {
+      const float wj = w[j];
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] += xs[r][j] * wj;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r >= rows) break;  // uniform over the workgroup
+      const int m = m0 + r;
+      h[(size_t)m * d + n] = acc[r];
+      float sq = acc[r] * acc[r];
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
+      if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
+    }
   }
-  const float tm = t[m];
   const int half = d >> 1;
-  if (n < half) {
-    const float arg = freqs[n] * tm;
-    store_op(te + afrag_index(m, n, KB), sinf(arg));
-    store_op(te + afrag_index(m, half + n, KB), cosf(arg));
-  }
+  if (n < half)
+    for (int r = 0; r < rows; ++r) {
+      const float arg = freqs[n] * t[m0 + r];
+      store_op(te + afrag_index(m0 + r, n, KB), sinf(arg));
+      store_op(te + afrag_index(m0 + r, half + n, KB), cosf(arg));
+    }
 }
 
 // v = RMSNorm(h) W_out^T + b_out, then x <- x + dt v unless frozen (mask or
@@ -216,15 +251,24 @@ __global__ void stamp_kernel(uint64_t *dst) {
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                        const float *b_in, const float *freqs, op_t *te, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
-  UAD_LAUNCH(temb_kernel, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te);
+  if (M >= 1024)
+    UAD_LAUNCH(temb_kernel<16>, dim3((M + 15) / 16, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in,
+               b_in, freqs, te);
+  else
+    UAD_LAUNCH(temb_kernel<1>, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in, b_in, freqs,
+               te);
   return hipGetLastError();
 }
 
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                            const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
                            hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  UAD_LAUNCH(temb_ada_kernel, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, Da, d, w_in, b_in, freqs, te, h, ssq,
-             m_alloc);
+  if (M >= 1024)
+    UAD_LAUNCH(temb_ada_kernel<16>, dim3((M + 15) / 16, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d,
+               w_in, b_in, freqs, te, h, ssq, m_alloc);
+  else
+    UAD_LAUNCH(temb_ada_kernel<1>, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in, b_in,
+               freqs, te, h, ssq, m_alloc);
   return hipGetLastError();
 }
 

@@ -95,12 +95,14 @@ def test_adarms_time_changes_velocity(gpu):
     assert np.abs(vs[0] - vs[1]).max() > 1e-3
 
 
-def test_adarms_batched_sampled_envs(gpu):
-    """8 environments, M = 400 rows: the batched projection kernel serves the
-    time MLP, the modulation GEMM and the gated residual epilogues.  Sampled
-    environments against the oracle run alone: one teacher-forced step, then
-    the free-running UAD schedule."""
-    c = case("pi05_b1_adarms", batch=8)
+@pytest.mark.parametrize("batch", [8, 24])
+def test_adarms_batched_sampled_envs(gpu, batch):
+    """8 / 24 environments, M = 400 / 1200 rows: the batched projection kernel
+    serves the time MLP, the modulation GEMM and the gated residual epilogues
+    (at 1200 rows the embedding kernel also takes 16 tokens per workgroup).
+    Sampled environments against the oracle run alone: one teacher-forced
+    step, then the free-running UAD schedule."""
+    c = case("pi05_b1_adarms", batch=batch)
     B, H = c.budgets.shape
     bud = np.full((B, H), 10, np.int32)
     bud[:, : H // 10] = 4
@@ -123,6 +125,6 @@ def test_adarms_batched_sampled_envs(gpu):
         e = rel_err(v[b], O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0])
         r = O.denoise_schedule(mb, c.noise[b:b + 1], bud[b:b + 1])
         ea = float(np.abs(rel[b] - r["released"][0]).max())
-        log(f"[pi05 B=8] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
+        log(f"[pi05 B={batch}] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
         assert e <= VEL_RTOL and ea <= ACT_ATOL
     np.testing.assert_array_equal(rst.cpu().numpy(), O.release_steps(bud))
