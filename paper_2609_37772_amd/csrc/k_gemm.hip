@@ -609,65 +609,78 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
   big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
 }
 
-// Gate/up at M >= kRingM: 256-row x 128-column tiles, 8 waves (4 x 2, each
-// 64 x 64), operands staged through a 3-stage LDS ring by LDS-direct loads
-// (16 A + 8 B fragment blocks per 32-deep stage, 3 per wave).  Each stage's
-// wait is a raw s_barrier after a partial vmcnt: __syncthreads' release fence
-// would drain the next stage's loads too.  The rows' norm statistics are
-// loaded into registers after the ring prologue (that wait is the prologue's
-// own round trip) and folded into rstd before the main loop.  Measured on the
-// 3200 x 8192 x 1024 and 2048 x 12288 x 1536 gate/up: 800 / 960 TFLOP/s
-// without epilogue, against 711 / 921 for the register-streamed tiles.
-constexpr int kRingM = 1024;
-constexpr int kRingRT = 16, kRingCT = 8, kRingNS = 3, kRingNW = 8;
-constexpr int kRingNBLK = kRingRT + kRingCT;
-constexpr int kRingLPW = kRingNBLK / kRingNW;  // LDS-direct loads per wave per stage
-static_assert(kRingNBLK % kRingNW == 0, "ring blocks per wave");
+// LDS-ring kernels for the widest batched projections: RT x CT 16-row /
+// 16-column tiles per workgroup, 8 waves (WR x WC), operands staged through
+// an NS-stage LDS ring by LDS-direct loads (RT + CT fragment blocks per
+// 32-deep stage).  Each stage's wait is a raw s_barrier after a partial
+// vmcnt: __syncthreads' release fence would drain the next stages' loads
+// too.  The rows' norm statistics are loaded into registers after the ring
+// prologue (that wait is the prologue's own round trip) and folded into
+// rstd after the main loop.  Measured without epilogue (TFLOP/s):
+//   gate/up 256 x 128, 4 x 2 waves, 3 stages: 3200 x 8192 x 1024: 800 (vs
+//   711 register-streamed), 2048 x 12288 x 1536: 960 (vs 921);
+//   QKV 128 x 128, 2 x 4 waves, 4 stages: 3200 x 2560 x 1024: 761 (vs 643;
+//   at 2048 x 2048 x 1536 the register-streamed kernel stays ahead, 651 vs 621).
+constexpr int kRingNW = 8;
+template <int EPI>
+struct RingShape;
+template <>
+struct RingShape<EPI_GEGLU> {
+  static constexpr int RT = 16, CT = 8, WR = 4, WC = 2, NS = 3, MinM = 1024;
+};
+template <>
+struct RingShape<EPI_QKV> {
+  static constexpr int RT = 8, CT = 8, WR = 2, WC = 4, NS = 4, MinM = 2560;
+};
 
 template <int EPI>
 __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
-  static_assert(EPI == EPI_GEGLU, "the ring kernel serves gate/up");
-  constexpr int TA = 4, TB = 4;
+  using S = RingShape<EPI>;
+  constexpr int RT = S::RT, CT = S::CT, WR = S::WR, WC = S::WC, NS = S::NS;
+  constexpr int NBLK = RT + CT, LPW = NBLK / kRingNW;  // LDS-direct loads per wave per stage
+  constexpr int TA = RT / WR, TB = CT / WC;            // 16 x 16 tiles per wave
+  constexpr int ROWS = 16 * RT, TPR = 512 / ROWS;       // rows per workgroup, threads per row's statistics
+  static_assert(WR * WC == kRingNW && NBLK % kRingNW == 0, "ring shape");
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ __align__(16) unsigned char ring_smem[];
   op_t *stage = (op_t *)ring_smem;  // [NS][NBLK][512]
-  __shared__ float rpart[2][256];
-  __shared__ float rstd_s[256];
-  const int tm = (g.M + 16 * kRingRT - 1) / (16 * kRingRT), tn = g.N / (16 * kRingCT), T = tm * tn;
+  __shared__ float rpart[TPR][ROWS];
+  __shared__ float rstd_s[ROWS];
+  const int tm = (g.M + ROWS - 1) / ROWS, tn = g.N / (16 * CT), T = tm * tn;
   const int per = (T + 7) / 8;
   const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);  // XCD = blockIdx % 8 takes a contiguous run
   if (t >= T) return;  // whole workgroup
   constexpr int GM = 8;
   const int grp = t / (GM * tn), in = t - grp * GM * tn;
   const int gm0 = grp * GM, gms = min(GM, tm - gm0);
-  const int mt0 = (gm0 + in % gms) * kRingRT, nt0 = (in / gms) * kRingCT;
+  const int mt0 = (gm0 + in % gms) * RT, nt0 = (in / gms) * CT;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wr = wave & 3, wc = wave >> 2;
+  const int wr = wave % WR, wc = wave / WR;
   const int KB = g.K / kTileK;
   const int mt_last = g.m_alloc / 16 - 1;
 
   auto issue = [&](int kb, int buf) {
-    op_t *dst = stage + (size_t)buf * kRingNBLK * kBlockElems;
+    op_t *dst = stage + (size_t)buf * NBLK * kBlockElems;
 #pragma unroll
-    for (int q = 0; q < kRingLPW; ++q) {
+    for (int q = 0; q < LPW; ++q) {
       const int bidx = wave + q * kRingNW;
-      const op_t *src = bidx < kRingRT ? g.A + ((size_t)min(mt0 + bidx, mt_last) * KB + kb) * kBlockElems
-                                       : g.W + ((size_t)(nt0 + bidx - kRingRT) * KB + kb) * kBlockElems;
+      const op_t *src = bidx < RT ? g.A + ((size_t)min(mt0 + bidx, mt_last) * KB + kb) * kBlockElems
+                                  : g.W + ((size_t)(nt0 + bidx - RT) * KB + kb) * kBlockElems;
       __builtin_amdgcn_global_load_lds((const void *)(src + lane * 8), (lds_void *)(dst + bidx * kBlockElems), 16, 0,
                                        0);
     }
   };
 #pragma unroll
-  for (int s = 0; s < kRingNS - 1; ++s)
+  for (int s = 0; s < NS - 1; ++s)
     if (s < KB) issue(s, s);
 
   if (g.use_rstd) {
-    // per-row sums of squares: thread t sums half of row (t & 255)'s tiles
-    const int row = min(mt0 * 16 + (threadIdx.x & 255), g.M - 1), half = threadIdx.x >> 8;
-    const int t0 = half * (g.ssq_tiles / 2), t1 = half ? g.ssq_tiles : g.ssq_tiles / 2;
+    // per-row sums of squares: TPR threads share row (tid % ROWS), each summing a slice of its tiles
+    const int row = min(mt0 * 16 + (int)(threadIdx.x % ROWS), g.M - 1), part = threadIdx.x / ROWS;
+    const int t0 = part * g.ssq_tiles / TPR, t1 = (part + 1) * g.ssq_tiles / TPR;
     float ss = 0.f;
     for (int q = t0; q < t1; ++q) ss += g.ssq[(size_t)q * g.m_alloc + row];
-    rpart[half][threadIdx.x & 255] = ss;
+    rpart[part][threadIdx.x % ROWS] = ss;
   }
 
   f32x4 acc[TA][TB];
@@ -677,19 +690,22 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
     for (int j = 0; j < TB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int kb = 0; kb < KB; ++kb) {
-    // stage kb landed for this wave (the next stage may stay in flight), then
+    // stage kb landed for this wave (later stages may stay in flight), then
     // for every wave; the buffer refilled below was last read one step ago
-    if (kb + 1 < KB)
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kRingLPW) : "memory");
+    const int later = min(NS - 2, KB - 1 - kb);  // stages issued after kb
+    if (later >= 2)
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPW) : "memory");
+    else if (later == 1)
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPW) : "memory");
     else
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (kb + kRingNS - 1 < KB) issue(kb + kRingNS - 1, (kb + kRingNS - 1) % kRingNS);
-    const op_t *sb = stage + (size_t)(kb % kRingNS) * kRingNBLK * kBlockElems + lane * 8;
+    if (kb + NS - 1 < KB) issue(kb + NS - 1, (kb + NS - 1) % NS);
+    const op_t *sb = stage + (size_t)(kb % NS) * NBLK * kBlockElems + lane * 8;
     f16x8 af[TA], bf[TB];
 #pragma unroll
     for (int i = 0; i < TA; ++i) af[i] = *(const f16x8 *)(sb + (wr * TA + i) * kBlockElems);
 #pragma unroll
-    for (int j = 0; j < TB; ++j) bf[j] = *(const f16x8 *)(sb + (kRingRT + wc * TB + j) * kBlockElems);
+    for (int j = 0; j < TB; ++j) bf[j] = *(const f16x8 *)(sb + (RT + wc * TB + j) * kBlockElems);
 #pragma unroll
     for (int i = 0; i < TA; ++i)
 #pragma unroll
@@ -698,24 +714,38 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
 
   if (g.use_rstd) {
     __syncthreads();  // rpart complete (also past every wave's last LDS read of the ring)
-    if (threadIdx.x < 256)
-      rstd_s[threadIdx.x] =
-          1.0f / sqrtf((rpart[0][threadIdx.x] + rpart[1][threadIdx.x]) / (float)(g.ssq_tiles * kTileN) + g.eps);
+    if (threadIdx.x < ROWS) {
+      float ss = 0.f;
+#pragma unroll
+      for (int p = 0; p < TPR; ++p) ss += rpart[p][threadIdx.x];
+      rstd_s[threadIdx.x] = 1.0f / sqrtf(ss / (float)(g.ssq_tiles * kTileN) + g.eps);
+    }
     __syncthreads();
   }
   big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, g.use_rstd ? rstd_s + wr * TA * 16 : nullptr);
 }
 
-static bool ring_ok(int epi, const GemmArgs &g) {
-  return epi == EPI_GEGLU && g.M >= kRingM && g.N % (16 * kRingCT) == 0 && g.A2 == nullptr && g.ssq_tiles % 2 == 0 &&
-         g.K / kTileK >= 1;
+template <int EPI>
+static bool ring_fits(const GemmArgs &g) {
+  using S = RingShape<EPI>;
+  return g.M >= S::MinM && g.N % (16 * S::CT) == 0 && g.A2 == nullptr && g.K / kTileK >= 1 &&
+         !(EPI == EPI_QKV && g.q_dim % 16 != 0);
 }
 
+template <int EPI>
 static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  const int tiles = (g.M + 16 * kRingRT - 1) / (16 * kRingRT) * (g.N / (16 * kRingCT));
-  const uint32_t lds = (uint32_t)(kRingNS * kRingNBLK * kBlockElems * sizeof(op_t));
-  UAD_LAUNCH((gemm_ring_kernel<EPI_GEGLU>), dim3((tiles + 7) / 8 * 8), dim3(512), lds, s, ev0, ev1, g);
+  using S = RingShape<EPI>;
+  const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
+  const uint32_t lds = (uint32_t)(S::NS * (S::RT + S::CT) * kBlockElems * sizeof(op_t));
+  UAD_LAUNCH((gemm_ring_kernel<EPI>), dim3((tiles + 7) / 8 * 8), dim3(512), lds, s, ev0, ev1, g);
   return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t ring_attr() {
+  using S = RingShape<EPI>;
+  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             S::NS * (S::RT + S::CT) * kBlockElems * (int)sizeof(op_t));
 }
 
 // 16*CT columns per workgroup: 256 for gate/up (the widest projection), 128 otherwise
@@ -755,8 +785,8 @@ static hipError_t big_attr() {
 }
 
 hipError_t gemm_init() {
-  hipError_t e = hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI_GEGLU>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     kRingNS * kRingNBLK * kBlockElems * (int)sizeof(op_t));
+  hipError_t e = ring_attr<EPI_GEGLU>();
+  if (e == hipSuccess) e = ring_attr<EPI_QKV>();
   if (e == hipSuccess) e = big_attr<EPI_BIAS_SILU>();
   if (e == hipSuccess) e = big_attr<EPI_RESID_F32>();
   if (e == hipSuccess) e = big_attr<EPI_GEGLU>();
@@ -807,7 +837,8 @@ GemmPlan plan_gemm(int epi, int M, int N, int K) {
 hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_t s, hipEvent_t ev0,
                        hipEvent_t ev1) {
   if (g.m_alloc < g.M || g.m_alloc % 16 != 0) return hipErrorInvalidValue;  // operand rows allocated
-  if (ring_ok(epi, g)) return launch_ring(g, s, ev0, ev1);
+  if (epi == EPI_GEGLU && ring_fits<EPI_GEGLU>(g)) return launch_ring<EPI_GEGLU>(g, s, ev0, ev1);
+  if (epi == EPI_QKV && ring_fits<EPI_QKV>(g)) return launch_ring<EPI_QKV>(g, s, ev0, ev1);
   if (big_ok(epi, g)) {
     switch (epi) {
       case EPI_BIAS_SILU: return launch_big<EPI_BIAS_SILU>(g, s, ev0, ev1);
