@@ -51,27 +51,6 @@ constexpr int attn_chunk_blocks() {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Reductions over lane pairs (l, l ^ 16) and (l, l ^ 32) with the gfx950
-// lane-swap instructions: swapping a value with itself leaves every lane its
-// own value and its partner's (lane layout checked by an in-bounds probe), so
-// no LDS-crossbar permute is needed (those showed up as LDS bank-conflict
-// cycles, 64 per key block and wave, in the attention's softmax).
-__device__ __forceinline__ float max_pair16(float v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float max_pair32(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float sum_pair16(float v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float sum_pair32(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
 
 // Workgroup wg of pf.wgs reads its 4 KiB-aligned share of the prefetch ranges
 // (16 bytes per lane per load, 8 loads in flight per lane: measured best of

@@ -79,8 +79,7 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
       ((float *)g.out)[(size_t)row * g.ldo + col] = hv;
     }
     float sq = hv * hv;  // sum over the 16 columns of this row (lanes sharing ln>>4)
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
+    sq = sum_row16(sq);
     if (row_ok) {
       if ((ln & 15) == 0) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
       if (g.mod_scale_next || g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * sc);
@@ -420,8 +419,7 @@ __device__ __forceinline__ void big_resid_rows(const GemmArgs &g, f32x4 (&acc)[T
       const f32x4 hv = h0[ii][j] + gt[ii][j] * acc[i0 + ii][j];
       if (row_ok) st4(h + (size_t)row * g.ldo + col, hv);
       float sq = hv[0] * hv[0] + hv[1] * hv[1] + hv[2] * hv[2] + hv[3] * hv[3];
-      sq += __shfl_xor(sq, 16);  // the 4 lanes holding this row's 16 columns
-      sq += __shfl_xor(sq, 32);
+      sq = sum_pair32(sum_pair16(sq));  // the 4 lanes holding this row's 16 columns
       if (row_ok) {
         if (lane < 16) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
         if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ii][j]);

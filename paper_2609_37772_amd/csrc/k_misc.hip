@@ -8,8 +8,7 @@ namespace uad {
 
 // Sum over a 256-thread block in a fixed order (wave shuffles, then 4 partials).
 __device__ __forceinline__ float block_sum_256(float v, float *scratch) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  v = sum_wave64(v);
   const int wave = threadIdx.x >> 6;
   __syncthreads();
   if ((threadIdx.x & 63) == 0) scratch[wave] = v;
@@ -104,8 +103,7 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
       const int m = m0 + r;
       h[(size_t)m * d + n] = acc[r];
       float sq = acc[r] * acc[r];
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 16);
+      sq = sum_row16(sq);
       if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
     }
   }
@@ -163,8 +161,7 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
       acc[o] = 0.f;
 #pragma unroll
       for (int i = 0; i < NC; ++i) acc[o] += (hv[i] * rstd * gv[i] + sv[i]) * wv[o][i];
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) acc[o] += __shfl_xor(acc[o], off);
+      acc[o] = sum_wave64(acc[o]);
     }
     if (lane == 0)
 #pragma unroll

@@ -56,6 +56,43 @@ constexpr int kBlockElems = kTileN * kTileK;  // 512 fp16 = 1 KiB
 
 __device__ __forceinline__ void store_op(op_t *p, float v) { *p = (op_t)v; }
 
+// ---------------------------------------------------------------------------
+// Cross-lane reductions without the LDS crossbar (ds_bpermute): DPP within a
+// row of 16 lanes (quad permutes for lane ^ 1 and lane ^ 2, then the half-row
+// and row mirrors, which pair the remaining groups), and the gfx950 lane-swap
+// instructions across rows (swapping a value with itself leaves each lane its
+// own value and that of lane ^ 16 / lane ^ 32).  Every lane of the group ends
+// with the same (bitwise) result.  Lane layouts checked by in-bounds probes.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float sum_row16(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]: lane ^ 1
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]: lane ^ 2
+  v += dpp_f<0x141>(v);  // row_half_mirror: the other quad of the 8
+  v += dpp_f<0x140>(v);  // row_mirror: the other 8 of the 16
+  return v;
+}
+__device__ __forceinline__ float sum_pair16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_pair32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_pair16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_pair32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_wave64(float v) { return sum_pair32(sum_pair16(sum_row16(v))); }
+
 // Activation operands use the same fragment order as the weights: a
 // [rows][K] matrix (rows padded to 16) is stored as [rows/16][K/32][64][8],
 // element (r, c) at lane (r & 15) + 16 * ((c & 31) >> 3), slot c & 7, so a
