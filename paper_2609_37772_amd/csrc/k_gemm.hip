@@ -354,17 +354,34 @@ constexpr int kBigM = 256;
 constexpr int kBigRowTiles = 8;  // 128 rows per workgroup
 constexpr int kBigPD = 3;        // k-blocks in flight per wave
 
-template <int CT>
-__device__ __forceinline__ bool big_tile(const GemmArgs &g, int &mt0, int &nt0) {
-  const int tm = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles), tn = g.N / (16 * CT), T = tm * tn;
+// Output tile of workgroup blockIdx.x over ceil(M / rows) row panels and tn
+// column panels: XCD x = blockIdx % 8 takes a contiguous run of tiles,
+// column-major over groups of 8 row panels, so the workgroups sharing an L2
+// share weight and activation panels.  The grid has 8 * ceil(tiles / 8)
+// workgroups (grid_tile_wgs); false for the padding ones.
+__host__ __device__ __forceinline__ int grid_tile_wgs(int M, int rows, int tn) {
+  return ((M + rows - 1) / rows * tn + 7) / 8 * 8;
+}
+
+__device__ __forceinline__ bool grid_tile(int M, int rows, int tn, int &pm, int &pn) {
+  const int tm = (M + rows - 1) / rows, T = tm * tn;
   const int per = (T + 7) / 8;
-  const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);  // XCD = blockIdx % 8 takes tiles [x*per, (x+1)*per)
+  const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
   if (t >= T) return false;
   constexpr int GM = 8;
   const int grp = t / (GM * tn), in = t - grp * GM * tn;
   const int gm0 = grp * GM, gms = min(GM, tm - gm0);
-  mt0 = (gm0 + in % gms) * kBigRowTiles;
-  nt0 = (in / gms) * CT;
+  pm = gm0 + in % gms;
+  pn = in / gms;
+  return true;
+}
+
+template <int CT>
+__device__ __forceinline__ bool big_tile(const GemmArgs &g, int &mt0, int &nt0) {
+  int pm, pn;
+  if (!grid_tile(g.M, 16 * kBigRowTiles, g.N / (16 * CT), pm, pn)) return false;
+  mt0 = pm * kBigRowTiles;
+  nt0 = pn * CT;
   return true;
 }
 
@@ -380,34 +397,17 @@ __device__ __forceinline__ void st4h(op_t *p, f32x4 v) {
   *(f16x4 *)p = f16x4{(op_t)v[0], (op_t)v[1], (op_t)v[2], (op_t)v[3]};
 }
 
-// Residual epilogue over NI row tiles starting at i0: h = h0 (or bias) + gate * v,
-// per-16-column sums of squares of h, next operand fp16(h * scale).  All loads of
-// the block are issued before its first store (the h stores may alias h0 loads
-// of other rows, so the compiler would not hoist them).  ADA: gate and scale
-// are per-token modulations, else gate = 1 and scale = gain_next.
+// Residual epilogue, store half, over NI row tiles starting at i0: h = h0 (or
+// bias) + gate * v, per-16-column sums of squares of h, next operand
+// fp16(h * scale).  ADA: gate and scale are per-token modulations ([NI][TB]),
+// else gate = 1 and scale = gain_next (one row [1][TB]).
 template <int NI, bool ADA, int TA, int TB>
-__device__ __forceinline__ void big_resid_rows(const GemmArgs &g, f32x4 (&acc)[TA][TB], int i0, int mt, int nt,
-                                               int lane) {
+__device__ __forceinline__ void big_resid_store(const GemmArgs &g, const f32x4 (&acc)[TA][TB], int i0, int mt, int nt,
+                                                int lane, const f32x4 (&h0)[NI][TB],
+                                                const f32x4 (&gt)[ADA ? NI : 1][TB],
+                                                const f32x4 (&sc)[ADA ? NI : 1][TB], bool has_next) {
   float *h = (float *)g.out;
   const int csub = 4 * (lane >> 4);
-  const bool has_next = ADA ? g.mod_scale_next != nullptr : g.gain_next != nullptr;
-  f32x4 h0[NI][TB], gt[NI][TB], sc[NI][TB];
-#pragma unroll
-  for (int ii = 0; ii < NI; ++ii) {
-    const int rowc = min((mt + i0 + ii) * 16 + (lane & 15), g.M - 1);
-#pragma unroll
-    for (int j = 0; j < TB; ++j) {
-      const int col = (nt + j) * 16 + csub;
-      h0[ii][j] = ld4(g.bias ? g.bias + col : h + (size_t)rowc * g.ldo + col);
-      if (ADA) {
-        gt[ii][j] = ld4(g.mod_gate + (size_t)rowc * g.mod_ld + col);
-        sc[ii][j] = has_next ? ld4(g.mod_scale_next + (size_t)rowc * g.mod_ld + col) + 1.0f : f32x4{0.f, 0.f, 0.f, 0.f};
-      } else {
-        gt[ii][j] = f32x4{1.f, 1.f, 1.f, 1.f};
-        sc[ii][j] = has_next ? ld4(g.gain_next + col) : f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-    }
-  }
   const int KBn = g.N / kTileK;
 #pragma unroll
   for (int ii = 0; ii < NI; ++ii) {
@@ -416,16 +416,63 @@ __device__ __forceinline__ void big_resid_rows(const GemmArgs &g, f32x4 (&acc)[T
 #pragma unroll
     for (int j = 0; j < TB; ++j) {
       const int tile = nt + j, col = tile * 16 + csub;
-      const f32x4 hv = h0[ii][j] + gt[ii][j] * acc[i0 + ii][j];
+      const f32x4 hv = ADA ? h0[ii][j] + gt[ADA ? ii : 0][j] * acc[i0 + ii][j] : h0[ii][j] + acc[i0 + ii][j];
       if (row_ok) st4(h + (size_t)row * g.ldo + col, hv);
       float sq = hv[0] * hv[0] + hv[1] * hv[1] + hv[2] * hv[2] + hv[3] * hv[3];
       sq = sum_pair32(sum_pair16(sq));  // the 4 lanes holding this row's 16 columns
       if (row_ok) {
         if (lane < 16) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
-        if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ii][j]);
+        if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ADA ? ii : 0][j]);
       }
     }
   }
+}
+
+// Residual epilogue, load half: h0 (or the bias) of NI row tiles from i0, and
+// the scale (and, ADA, the gate) of the next operand.  Branch-free: every load
+// comes from a valid address (an absent operand is stood in for by one that
+// exists) and the value is selected afterwards, so no load waits on another.
+template <int NI, bool ADA, int TB>
+__device__ __forceinline__ void big_resid_load(const GemmArgs &g, int i0, int mt, int nt, int lane,
+                                               f32x4 (&h0)[NI][TB], f32x4 (&gt)[ADA ? NI : 1][TB],
+                                               f32x4 (&sc)[ADA ? NI : 1][TB]) {
+  const int csub = 4 * (lane >> 4);
+  const bool has_next = ADA ? g.mod_scale_next != nullptr : g.gain_next != nullptr;
+  const float *hb = g.bias ? g.bias : (const float *)g.out;
+  const size_t hld = g.bias ? 0 : (size_t)g.ldo;
+  const float *sb = ADA ? (has_next ? g.mod_scale_next : g.mod_gate) : (has_next ? g.gain_next : hb);
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ii = 0; ii < NI; ++ii) {
+    const int rowc = min((mt + i0 + ii) * 16 + (lane & 15), g.M - 1);
+#pragma unroll
+    for (int j = 0; j < TB; ++j) {
+      const int col = (nt + j) * 16 + csub;
+      h0[ii][j] = ld4(hb + (size_t)rowc * hld + col);
+      if (ADA) {
+        const size_t ro = (size_t)rowc * g.mod_ld + col;
+        gt[ADA ? ii : 0][j] = ld4(g.mod_gate + ro);
+        const f32x4 sv = ld4(sb + ro);
+        sc[ADA ? ii : 0][j] = has_next ? sv + 1.0f : zero;
+      } else if (ii == 0) {
+        gt[0][j] = f32x4{1.f, 1.f, 1.f, 1.f};
+        const f32x4 sv = ld4(sb + col);
+        sc[0][j] = has_next ? sv : zero;
+      }
+    }
+  }
+}
+
+// Residual epilogue over NI row tiles starting at i0, loads then stores.  All
+// loads of the block are issued before its first store (the h stores may alias
+// h0 loads of other rows, so the compiler would not hoist them).
+template <int NI, bool ADA, int TA, int TB>
+__device__ __forceinline__ void big_resid_rows(const GemmArgs &g, f32x4 (&acc)[TA][TB], int i0, int mt, int nt,
+                                               int lane) {
+  f32x4 h0[NI][TB], gt[ADA ? NI : 1][TB], sc[ADA ? NI : 1][TB];
+  big_resid_load<NI, ADA, TB>(g, i0, mt, nt, lane, h0, gt, sc);
+  const bool has_next = ADA ? g.mod_scale_next != nullptr : g.gain_next != nullptr;
+  big_resid_store<NI, ADA, TA, TB>(g, acc, i0, mt, nt, lane, h0, gt, sc, has_next);
 }
 
 template <int EPI, int TA, int TB>
@@ -542,7 +589,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
   extern __shared__ float ssq_s[];  // [ssq_tiles][128] sums of squares of the workgroup's rows when kRstd
   __shared__ float rstd_s[128];
   int mt0, nt0;
-  if (!big_tile<CT>(g, mt0, nt0)) return;  // whole workgroup: the grid is padded to a multiple of 8
+  if (!big_tile<CT>(g, mt0, nt0)) return;  // whole workgroup: padding of the grid
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wr = wave & 1, wc = wave >> 1;
   const int KB = g.K / kTileK;
@@ -604,7 +651,8 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
+  big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane,
+                            (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
 }
 
 // LDS-ring kernels for the widest batched projections: RT x CT 16-row /
@@ -644,14 +692,9 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   op_t *stage = (op_t *)ring_smem;  // [NS][NBLK][512]
   __shared__ float rpart[TPR][ROWS];
   __shared__ float rstd_s[ROWS];
-  const int tm = (g.M + ROWS - 1) / ROWS, tn = g.N / (16 * CT), T = tm * tn;
-  const int per = (T + 7) / 8;
-  const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);  // XCD = blockIdx % 8 takes a contiguous run
-  if (t >= T) return;  // whole workgroup
-  constexpr int GM = 8;
-  const int grp = t / (GM * tn), in = t - grp * GM * tn;
-  const int gm0 = grp * GM, gms = min(GM, tm - gm0);
-  const int mt0 = (gm0 + in % gms) * RT, nt0 = (in / gms) * CT;
+  int pm, pn;
+  if (!grid_tile(g.M, ROWS, g.N / (16 * CT), pm, pn)) return;  // whole workgroup
+  const int mt0 = pm * RT, nt0 = pn * CT;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wr = wave % WR, wc = wave / WR;
   const int KB = g.K / kTileK;
@@ -733,9 +776,9 @@ static bool ring_fits(const GemmArgs &g) {
 template <int EPI>
 static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   using S = RingShape<EPI>;
-  const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
+  const int wgs = grid_tile_wgs(g.M, 16 * S::RT, g.N / (16 * S::CT));
   const uint32_t lds = (uint32_t)(S::NS * (S::RT + S::CT) * kBlockElems * sizeof(op_t));
-  UAD_LAUNCH((gemm_ring_kernel<EPI>), dim3((tiles + 7) / 8 * 8), dim3(512), lds, s, ev0, ev1, g);
+  UAD_LAUNCH((gemm_ring_kernel<EPI>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
 
@@ -750,14 +793,30 @@ static hipError_t ring_attr() {
 template <int EPI>
 constexpr int big_ct() { return EPI == EPI_GEGLU ? 16 : 8; }
 
-template <int EPI>
-static hipError_t launch_big(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  constexpr int CT = big_ct<EPI>();
+static int g_n_cu = 256;  // compute units of the device (set by gemm_init)
+
+template <int EPI, int CT>
+static hipError_t launch_big_ct(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const bool rstd = (EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd;
   const size_t lds = rstd ? (size_t)g.ssq_tiles * 128 * 4 : 0;
-  const int tiles = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles) * (g.N / (16 * CT));
-  UAD_LAUNCH((gemm_big_kernel<EPI, CT>), dim3((tiles + 7) / 8 * 8), dim3(256), (uint32_t)lds, s, ev0, ev1, g);
+  const int wgs = grid_tile_wgs(g.M, 16 * kBigRowTiles, g.N / (16 * CT));
+  UAD_LAUNCH((gemm_big_kernel<EPI, CT>), dim3(wgs), dim3(256), (uint32_t)lds, s, ev0, ev1, g);
   return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_big(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if constexpr (EPI == EPI_RESID_F32) {
+    // Residual projections (N = d): 96-column tiles when they need fewer
+    // 16 x 16 output tiles per CU than 128-column ones (1536 wide, 2048 rows:
+    // 256 tiles of 48 instead of 192 tiles of 64 with 64 CUs idle).
+    auto per_cu = [&](int ct) {
+      const int tiles = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles) * (g.N / (16 * ct));
+      return (tiles + g_n_cu - 1) / g_n_cu * ct;
+    };
+    if (g.N % 96 == 0 && per_cu(6) < per_cu(8)) return launch_big_ct<EPI, 6>(g, s, ev0, ev1);
+  }
+  return launch_big_ct<EPI, big_ct<EPI>()>(g, s, ev0, ev1);
 }
 
 // The batched kernel serves M >= kBigM when the columns divide into its tiles,
@@ -783,7 +842,11 @@ static hipError_t big_attr() {
 }
 
 hipError_t gemm_init() {
-  hipError_t e = ring_attr<EPI_GEGLU>();
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&g_n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess && g_n_cu < 1) e = hipErrorInvalidDevice;
+  if (e == hipSuccess) e = ring_attr<EPI_GEGLU>();
   if (e == hipSuccess) e = ring_attr<EPI_QKV>();
   if (e == hipSuccess) e = big_attr<EPI_BIAS_SILU>();
   if (e == hipSuccess) e = big_attr<EPI_RESID_F32>();
