@@ -83,14 +83,17 @@ __device__ __forceinline__ void prefetch_share(const Prefetch &pf, int wg, unsig
 // LOWREG: the K fragments of each 16-key half and the V fragments of each
 // half of the output columns are read just before their MFMAs (fewer live
 // registers: two waves per SIMD at HD = 256) instead of all up front.
-template <int HD, int NB, bool LOWREG>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+// NW waves (16 query rows each) per workgroup; NW > 4 only without split-KV
+// (a.qblocks counts blocks of 16 * NW rows).
+template <int HD, int NB, bool LOWREG, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char attn_smem[];
   AttnBlock<HD> *bufs = (AttnBlock<HD> *)attn_smem;  // [2][NB]
   constexpr int KS = HD / 32;   // k-steps of the QK^T product
   constexpr int NTO = HD / 16;  // 16-column output tiles
   constexpr int CPR = HD / 8;   // 16-byte chunks per K row
-  constexpr int INS = HD / 64;  // LDS-direct instructions per wave per tile (4 waves x 64 lanes x 16 B)
+  constexpr int TI = HD / 16;   // LDS-direct instructions (64 lanes x 16 B) per K or V^T tile
+  constexpr int INS = (TI + NW - 1) / NW;  // per wave, the last ones guarded
   if ((int)blockIdx.x >= (int)gridDim.x - a.pre_attn.wgs) {  // prefetch workgroups follow the attention ones
     prefetch_share(a.pre_attn, blockIdx.x - (gridDim.x - a.pre_attn.wgs), a.pf_sink);
     return;
@@ -119,7 +122,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   if (blk1 > n_blocks) blk1 = n_blocks;
 
   // This lane's query (as the B operand of S^T): packed row r0 + (lane & 15).
-  const int r0 = qblock * 64 + wave * 16;
+  const int r0 = qblock * (16 * NW) + wave * 16;
   const int my_r = r0 + (lane & 15);
   bf16x8 qf[KS];
   {
@@ -143,7 +146,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       const __bf16 *vb = vbase + (size_t)blk * 32 * HD;
 #pragma unroll
       for (int i = 0; i < INS; ++i) {
-        const int q0 = (wave * INS + i) * 64;  // first LDS chunk of this instruction
+        if (TI % NW != 0 && wave + i * NW >= TI) break;  // wave-uniform
+        const int q0 = (wave + i * NW) * 64;  // first LDS chunk of this instruction
         const int q = q0 + lane;
         const int kr = q / CPR, kp = q - kr * CPR;
         __builtin_amdgcn_global_load_lds((const void *)(kb + kr * HD + ((kp ^ (kr & 7)) * 8)),
@@ -360,6 +364,8 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
   }
 }
 
+static int g_attn_cus = 256;  // compute units of the device (set by attention_init)
+
 template <int HD>
 static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int NB = attn_chunk_blocks<HD>();
@@ -375,10 +381,39 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
   // splits (batch 1): NB blocks per stage, one memory round trip per split.
   const bool streamed = a.blocks_per_split > 2 * NB;
   const uint32_t lds = (uint32_t)(2 * (streamed ? 1 : NB) * sizeof(AttnBlock<HD>));
+  if (streamed && a.splits == 1 && a.pre_attn.wgs == 0) {
+    // Without split-KV every workgroup of a group re-reads the group's whole
+    // K/V, so fewer, taller query blocks cut that traffic; 4-wave workgroups
+    // run two per CU, 6- and 8-wave ones one.  Take the row block that gives
+    // the fewest 16-row tasks on the busiest CU, then the fewest workgroups.
+    int best_nw = 4, best_load = 0, best_wgs = 0;
+    for (int nw : {4, 6, 7, 8}) {
+      const int wgs = groups * ((a.rows + 16 * nw - 1) / (16 * nw));
+      const int per_cu = nw == 4 ? 2 : 1;
+      const int load = (wgs + g_attn_cus * per_cu - 1) / (g_attn_cus * per_cu) * per_cu * nw;
+      if (nw == 4 || load < best_load || (load == best_load && wgs < best_wgs)) {
+        best_nw = nw;
+        best_load = load;
+        best_wgs = wgs;
+      }
+    }
+    if (best_nw != 4) {
+      AttnArgs at = a;
+      at.qblocks = (a.rows + 16 * best_nw - 1) / (16 * best_nw);
+      const dim3 g2(8 * ((groups + 7) / 8) * at.qblocks);
+      if (best_nw == 6)
+        UAD_LAUNCH((attn_kernel<HD, 1, true, 6>), g2, dim3(384), lds, s, ev0, end_attn, at);
+      else if (best_nw == 7)
+        UAD_LAUNCH((attn_kernel<HD, 1, true, 7>), g2, dim3(448), lds, s, ev0, end_attn, at);
+      else
+        UAD_LAUNCH((attn_kernel<HD, 1, true, 8>), g2, dim3(512), lds, s, ev0, end_attn, at);
+      return hipGetLastError();
+    }
+  }
   if (streamed)
-    UAD_LAUNCH((attn_kernel<HD, 1, true>), grid, dim3(256), lds, s, ev0, end_attn, a);
+    UAD_LAUNCH((attn_kernel<HD, 1, true, 4>), grid, dim3(256), lds, s, ev0, end_attn, a);
   else
-    UAD_LAUNCH((attn_kernel<HD, NB, false>), grid, dim3(256), lds, s, ev0, end_attn, a);
+    UAD_LAUNCH((attn_kernel<HD, NB, false, 4>), grid, dim3(256), lds, s, ev0, end_attn, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   hipEvent_t none = nullptr;
@@ -401,16 +436,30 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
 template <int HD>
 static hipError_t init_hd() {
   constexpr int NB = attn_chunk_blocks<HD>();
-  hipError_t e = hipFuncSetAttribute((const void *)attn_kernel<HD, NB, false>,
+  constexpr int streamed_lds = (int)(2 * sizeof(AttnBlock<HD>));
+  hipError_t e = hipFuncSetAttribute((const void *)attn_kernel<HD, NB, false, 4>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)(2 * NB * sizeof(AttnBlock<HD>)));
   if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)(2 * sizeof(AttnBlock<HD>)));
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 4>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            streamed_lds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 6>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            streamed_lds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 7>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            streamed_lds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            streamed_lds);
   return e;
 }
 
 hipError_t attention_init() {
-  hipError_t e = init_hd<64>();
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&g_attn_cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess && g_attn_cus < 1) e = hipErrorInvalidDevice;
+  if (e == hipSuccess) e = init_hd<64>();
   if (e == hipSuccess) e = init_hd<128>();
   if (e == hipSuccess) e = init_hd<256>();
   return e;
