@@ -144,10 +144,12 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
       AttnBlock<HD> &dst = bufs[which * NB + j];
       const __bf16 *kb = kbase + (size_t)blk * 32 * HD;
       const __bf16 *vb = vbase + (size_t)blk * 32 * HD;
+      // wave w issues the contiguous instructions [w*TI/NW, (w+1)*TI/NW)
+      const int ins0 = wave * TI / NW, ins1 = (wave + 1) * TI / NW;
 #pragma unroll
       for (int i = 0; i < INS; ++i) {
-        if (TI % NW != 0 && wave + i * NW >= TI) break;  // wave-uniform
-        const int q0 = (wave + i * NW) * 64;  // first LDS chunk of this instruction
+        if (TI % NW != 0 && ins0 + i >= ins1) break;  // wave-uniform
+        const int q0 = (ins0 + i) * 64;  // first LDS chunk of this instruction
         const int q = q0 + lane;
         const int kr = q / CPR, kp = q - kr * CPR;
         __builtin_amdgcn_global_load_lds((const void *)(kb + kr * HD + ((kp ^ (kr & 7)) * 8)),
