@@ -205,9 +205,12 @@ uad_status uad_denoise_schedule(uad_ctx *ctx, float *x, const float *t_sched, co
  *   gac_mask      device uint8 [Da] or NULL: 1 = additive dimension corrected,
  *                 0 = left as denoised (e.g. a gripper); NULL corrects all
  *   urgent_host   pinned host fp32 [batch][U][Da] or NULL: receives a copy of
- *                 the urgent actions on a separate release stream as soon as
- *                 step K is done, while the tail keeps denoising on the
- *                 context's stream (App. C, asynchronous execution)
+ *                 the urgent actions as soon as step K is done, while the
+ *                 tail keeps denoising on the context's stream (App. C,
+ *                 asynchronous execution).  Page-locked memory (hipHostMalloc,
+ *                 torch pin_memory) is written by the release kernel itself
+ *                 through its device address; other host memory gets a copy
+ *                 on a separate release stream (slower)
  *   release_event hipEvent_t or NULL: recorded when the urgent actions (and
  *                 their host copy, if requested) are final; a controller waits
  *                 on it instead of on the whole chunk

@@ -215,9 +215,12 @@ __global__ __launch_bounds__(256) void tr_release_kernel(TrArgs a) {
     const int bu = i / a.Da;
     const int b = bu / a.U, u = bu - b * a.U;
     const size_t idx = ((size_t)b * a.H + u) * a.Da + c;
-    a.urgent[i] = a.x[idx];
+    const float v = a.x[idx];
+    a.urgent[i] = v;
+    if (a.urgent_host) a.urgent_host[i] = v;  // straight to the controller's pinned buffer
     if (a.reconcile) a.x[idx] = a.x0[idx] + a.dt_star * a.vsum[idx];
   }
+  if (a.urgent_host) __threadfence_system();
 }
 
 // Ghost Action Correction (Sec. 4.4): E = sum_{i<U} (a'^i - a^i) over the ghost

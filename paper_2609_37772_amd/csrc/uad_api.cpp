@@ -790,6 +790,7 @@ static uad_status enqueue_release_phase(uad_ctx *c, hipStream_t s, const GraphKe
   TrArgs a{};
   a.x = k.x; a.x0 = c->tr_x0; a.vsum = c->tr_vsum; a.urgent = k.urgent; a.executed = k.executed;
   a.gac_mask = k.gac_mask; a.B = k.B; a.H = k.H; a.Da = c->Da; a.U = k.U; a.S = k.S;
+  a.urgent_host = k.kind == 1 ? k.urgent_host : nullptr;
   a.dt_star = -(1.0f / (float)k.Nstar); a.reconcile = k.reconcile;
   hipError_t e = hipSuccess;
   const int st0 = k.kind == 1 ? 0 : k.Kr, st1 = k.kind == 1 ? k.Kr : k.Nstar;
@@ -944,17 +945,29 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
     if (e != hipSuccess) return hip_fail(c, e, "uad_denoise_release: step tables");
     std::copy(key, key + 6, c->tr_key);
   }
+  // Pinned urgent_host: the release kernel writes it through its device
+  // address (a cross-stream copy after the release cost ~90 us of the time to
+  // first release at batch 1); other host memory is copied on the release stream.
+  // (looked up on every call: a freed pinned buffer's address may come back as pageable memory)
+  float *host_dev = nullptr;
+  if (urgent_host) {
+    hipPointerAttribute_t pa{};
+    if (hipPointerGetAttributes(&pa, urgent_host) == hipSuccess && pa.type == hipMemoryTypeHost && pa.devicePointer)
+      host_dev = (float *)pa.devicePointer;
+    (void)hipGetLastError();  // pageable memory: the query's error is expected
+  }
   GraphKey k{};
   k.kind = 1;
   k.x = x; k.B = batch; k.H = chunk; k.n_steps = Nstar; k.step_ticks = step_ticks;
   k.U = U; k.Kr = K; k.Nstar = Nstar; k.S = S; k.reconcile = reconcile;
-  k.urgent = urgent_out; k.executed = executed_out; k.gac_mask = gac_mask;
+  k.urgent = urgent_out; k.executed = executed_out; k.gac_mask = gac_mask; k.urgent_host = host_dev;
   uad_status rs = run_work(c, k);
   if (rs != UAD_OK) return rs;
-  // release: the urgent actions are final here; copy them to the host on the
-  // release stream while the tail continues on the context stream
+  // release: the urgent actions (and their pinned host copy) are final here;
+  // a pageable host buffer gets its copy on the release stream while the
+  // tail continues on the context stream
   hipError_t e = hipEventRecord(c->ev_rel, c->stream);
-  if (e == hipSuccess && urgent_host) {
+  if (e == hipSuccess && urgent_host && !host_dev) {
     e = hipStreamWaitEvent(c->rel_stream, c->ev_rel, 0);
     if (e == hipSuccess)
       e = hipMemcpyAsync(urgent_host, urgent_out, (size_t)batch * U * c->Da * sizeof(float), hipMemcpyDeviceToHost,
@@ -965,6 +978,7 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
   }
   if (e != hipSuccess) return hip_fail(c, e, "uad_denoise_release: release");
   k.kind = 2;
+  k.urgent_host = nullptr;
   return run_work(c, k);
 }
 

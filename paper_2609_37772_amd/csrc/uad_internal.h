@@ -231,6 +231,7 @@ struct TrArgs {
   float *urgent;         // [B][U][Da] released urgent actions x_K
   float *executed;       // [B][S][Da] urgent actions then GAC-corrected tail, or null
   const uint8_t *gac_mask;  // [Da] 1 = additive dimension corrected, or null (all)
+  float *urgent_host;    // device address of pinned host [B][U][Da] that also receives them, or null
   int B, H, Da, U, S;
   float dt_star;         // -(1/N*), the canonical step
   int reconcile;         // 1: TR (ghosts continue), 0: plain early release (urgent frozen)
@@ -288,9 +289,10 @@ struct GraphKey {
   int U, Kr, Nstar, S, reconcile;
   float *urgent, *executed;
   const uint8_t *gac_mask;
+  float *urgent_host;  // device address of the pinned host copy written by the release kernel, or null
   bool operator==(const GraphKey &o) const {
     return kind == o.kind && U == o.U && Kr == o.Kr && Nstar == o.Nstar && S == o.S && reconcile == o.reconcile &&
-           urgent == o.urgent && executed == o.executed && gac_mask == o.gac_mask &&
+           urgent == o.urgent && executed == o.executed && gac_mask == o.gac_mask && urgent_host == o.urgent_host &&
            is_schedule == o.is_schedule && x == o.x && t == o.t && dt == o.dt && mask == o.mask &&
            v_out == o.v_out && released == o.released && release_step == o.release_step &&
            step_ticks == o.step_ticks && n_steps == o.n_steps && B == o.B && H == o.H &&
@@ -355,7 +357,7 @@ struct uad_ctx {
   float *tr_t = nullptr, *tr_dt = nullptr;     // [kMaxSteps][m_alloc] step tables of the last configuration
   uint8_t *tr_mask = nullptr;
   int tr_key[6] = {0, 0, 0, 0, 0, -1};         // B, H, U, K, N*, reconcile of the tables
-  hipStream_t rel_stream = nullptr;            // release copies
+  hipStream_t rel_stream = nullptr;            // release copies to pageable host memory
   hipEvent_t ev_rel = nullptr;
 
   // captured step / schedule graphs (small LRU cache)
