@@ -340,11 +340,14 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
     const size_t tile = ((size_t)min(sp, splits - 1) * n_eh + eh) * ntiles + rt;
     const f16x4 ov = *(const f16x4 *)(a.opart + tile * (16 * (size_t)hd) + nt * 256 + lane * 4);
     os[sp] = sp < splits ? ov : f16x4{};
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float2 v = *(const float2 *)(a.mlpart + (tile * 16 + rbase + r) * 2);
-      ml[sp][r] = sp < splits ? v : float2{-INFINITY, 0.f};
-    }
+    // the (m, l) pairs of this lane's 4 rows are 32 contiguous bytes: two 16-byte loads
+    const f32x4 *mp = (const f32x4 *)(a.mlpart + (tile * 16 + rbase) * 2);
+    const f32x4 v01 = mp[0], v23 = mp[1];
+    const bool ok = sp < splits;
+    ml[sp][0] = ok ? float2{v01[0], v01[1]} : float2{-INFINITY, 0.f};
+    ml[sp][1] = ok ? float2{v01[2], v01[3]} : float2{-INFINITY, 0.f};
+    ml[sp][2] = ok ? float2{v23[0], v23[1]} : float2{-INFINITY, 0.f};
+    ml[sp][3] = ok ? float2{v23[2], v23[3]} : float2{-INFINITY, 0.f};
   }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {

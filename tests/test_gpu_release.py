@@ -136,6 +136,36 @@ def test_async_release_to_pinned_host(gpu):
     assert np.all(np.diff(tk) > 0), "step ticks must increase"
 
 
+def test_release_to_pageable_host_through_c_abi(gpu):
+    """Host memory that is not page-locked (a NumPy array) takes the copy on
+    the release stream instead of the release kernel's direct stores: the
+    values still equal the device copy bit for bit, and the pinned path on
+    the same context still works afterwards."""
+    import ctypes
+    c = case("tiny")
+    B, H, Da = c.noise.shape
+    U_, K, Ns, S = 4, 2, 5, 10
+    lib = U.load_library()
+    x = dev(c.noise.astype(np.float32))
+    urgent = torch.empty((B, U_, Da), device="cuda")
+    host = np.full((B, U_, Da), np.nan, np.float32)
+    vp = ctypes.c_void_p
+    st = lib.uad_denoise_release(c.expert.ctx, vp(x.data_ptr()), B, H, U_, K, Ns, S, U.UAD_RELEASE_TR,
+                                 vp(urgent.data_ptr()), None, None, vp(host.ctypes.data), None, None)
+    assert st == 0
+    torch.cuda.synchronize()  # the release stream's copy included
+    assert np.array_equal(host, urgent.cpu().numpy())
+    pinned = torch.full((B, U_, Da), float("nan")).pin_memory()
+    ev = torch.cuda.Event()
+    x2 = dev(c.noise.astype(np.float32))
+    c.expert.release(x2, U_, K, Ns, S, urgent=urgent, urgent_host=pinned, release_event=ev)
+    ev.synchronize()
+    got = pinned.clone()
+    torch.cuda.synchronize()
+    assert torch.equal(got, urgent.cpu())
+    assert np.array_equal(host, got.numpy())  # same inputs, same release
+
+
 def test_release_costs_exactly_nstar_evaluations(gpu):
     """TR needs no extra F_theta evaluations (Sec. 4.3): N* joint steps in total."""
     c = case("tiny")
