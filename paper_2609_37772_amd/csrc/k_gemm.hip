@@ -156,7 +156,8 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
     const op_t *ap = g.A + ((size_t)mt0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
     for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
-      const bool ok = mt < nmt && (m0 + mt * 16 + (lane & 15)) < g.M;
+      if (mt >= nmt) break;  // wave-uniform: no instructions for the group's absent row tiles
+      const bool ok = (m0 + mt * 16 + (lane & 15)) < g.M;
 #pragma unroll
       for (int j = 0; j < KPW; ++j) a[j][mt] = ok ? *(const f16x8 *)(ap + ((size_t)mt * KB + j) * kBlockElems) : f16x8{};
       if (DUAL) {
@@ -257,11 +258,13 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   // Cross-wave reduction through LDS, fixed order over waves.
   constexpr int SLOTS = kMaxTilesPerGroup * T * 4;  // (mt, t, r) triples per lane
 #pragma unroll
-  for (int mt = 0; mt < kMaxTilesPerGroup; ++mt)
+  for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
+    if (mt >= nmt) break;  // the epilogue reads only the group's own row tiles
 #pragma unroll
     for (int t = 0; t < T; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[((wave * SLOTS) + (mt * T + t) * 4 + r) * 64 + lane] = acc[mt][t][r];
+  }
   __syncthreads();
   if (!DUAL && kRstd && g.use_rstd && threadIdx.x < 64) {
     float ss = 0.f;
