@@ -118,3 +118,28 @@ def test_mid_batch_sampled_envs(gpu):
         log(f"[pi0 B=8] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
         assert e <= VEL_RTOL and ea <= ACT_ATOL
     np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
+
+
+def test_tall_query_blocks_sampled_envs(gpu):
+    """40 environments of the small model with a 128-token chunk and a 256-token
+    prefix (12 key blocks, no split-KV): the attention runs 8-wave workgroups
+    of 128 query rows, one per (environment, KV head); the other row-block
+    sizes are covered by the fleet (7 waves) and the large expert (6).
+    Sampled environments against the oracle run alone."""
+    c = case("tiny", batch=40, chunk=128, prefix=256)
+    B, H = c.budgets.shape
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    xg = dev(c.noise.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)), dev(mask[0].astype(np.uint8)), vg)
+    torch.cuda.synchronize()
+    v = vg.cpu().numpy()
+    _, x, rel, rst = schedule_gpu(c, c.budgets)
+    for b in (0, 23, B - 1):
+        mb = c.oracle_model([b])
+        e = rel_err(v[b], O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0])
+        r = O.denoise_schedule(mb, c.noise[b:b + 1], c.budgets[b:b + 1])
+        ea = float(np.abs(rel[b] - r["released"][0]).max())
+        log(f"[tiny B=40 H=128] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
+        assert e <= VEL_RTOL and ea <= ACT_ATOL
+    np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
