@@ -584,10 +584,14 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
   }
 }
 
-template <int EPI, int CT>
+// DUAL (adaptive norm, QKV / gate-up): a second accumulator takes A2 W (the
+// norm's shift through the weights) and is added after the rows' rstd has
+// scaled the first: rstd * (A W) + A2 W.
+template <int EPI, int CT, bool DUAL = false>
 __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
   constexpr int TA = kBigRowTiles / 2, TB = CT / 2, PD = kBigPD;
   constexpr bool kRstd = (EPI == EPI_QKV || EPI == EPI_GEGLU);
+  static_assert(!DUAL || kRstd, "the second operand belongs to a normalised projection");
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ float ssq_s[];  // [ssq_tiles][128] sums of squares of the workgroup's rows when kRstd
   __shared__ float rstd_s[128];
@@ -611,7 +615,12 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
   for (int i = 0; i < TA; ++i) pa[i] = g.A + (size_t)min(mt0 + wr * TA + i, mt_last) * KB * kBlockElems + lane * 8;
 #pragma unroll
   for (int j = 0; j < TB; ++j) pb[j] = g.W + (size_t)(nt0 + wc * TB + j) * KB * kBlockElems + lane * 8;
-  f16x8 ra[PD][TA], rb[PD][TB];
+  constexpr int TA2 = DUAL ? TA : 1;
+  const op_t *pa2[TA2];
+#pragma unroll
+  for (int i = 0; i < TA2; ++i)
+    pa2[i] = DUAL ? g.A2 + (size_t)min(mt0 + wr * TA + i, mt_last) * KB * kBlockElems + lane * 8 : nullptr;
+  f16x8 ra[PD][TA], rb[PD][TB], ra2[PD][TA2];
 #pragma unroll
   for (int s = 0; s < PD; ++s) {
     const int kb = min(s, KB - 1);
@@ -619,12 +628,20 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
     for (int i = 0; i < TA; ++i) ra[s][i] = *(const f16x8 *)(pa[i] + (size_t)kb * kBlockElems);
 #pragma unroll
     for (int j = 0; j < TB; ++j) rb[s][j] = *(const f16x8 *)(pb[j] + (size_t)kb * kBlockElems);
+    if constexpr (DUAL)
+#pragma unroll
+      for (int i = 0; i < TA; ++i) ra2[s][i] = *(const f16x8 *)(pa2[i] + (size_t)kb * kBlockElems);
   }
-  f32x4 acc[TA][TB];
+  f32x4 acc[TA][TB], acc2[TA2][DUAL ? TB : 1];
 #pragma unroll
   for (int i = 0; i < TA; ++i)
 #pragma unroll
     for (int j = 0; j < TB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (DUAL)
+#pragma unroll
+    for (int i = 0; i < TA; ++i)
+#pragma unroll
+      for (int j = 0; j < TB; ++j) acc2[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int k0 = 0; k0 < KB; k0 += PD) {
 #pragma unroll
     for (int s = 0; s < PD; ++s) {
@@ -632,14 +649,20 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
 #pragma unroll
         for (int i = 0; i < TA; ++i)
 #pragma unroll
-          for (int j = 0; j < TB; ++j)
+          for (int j = 0; j < TB; ++j) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(rb[s][j], ra[s][i], acc[i][j], 0, 0, 0);
+            if constexpr (DUAL)
+              acc2[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(rb[s][j], ra2[s][i], acc2[i][j], 0, 0, 0);
+          }
       }
       const int kb = min(k0 + s + PD, KB - 1);  // past the end: re-load the last block (never used)
 #pragma unroll
       for (int i = 0; i < TA; ++i) ra[s][i] = *(const f16x8 *)(pa[i] + (size_t)kb * kBlockElems);
 #pragma unroll
       for (int j = 0; j < TB; ++j) rb[s][j] = *(const f16x8 *)(pb[j] + (size_t)kb * kBlockElems);
+      if constexpr (DUAL)
+#pragma unroll
+        for (int i = 0; i < TA; ++i) ra2[s][i] = *(const f16x8 *)(pa2[i] + (size_t)kb * kBlockElems);
     }
   }
 
@@ -654,8 +677,19 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane,
-                            (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
+  if constexpr (DUAL) {
+    // lane l of tile (i, j) holds row l & 15 (swapped operands)
+#pragma unroll
+    for (int i = 0; i < TA; ++i) {
+      const float rs = rstd_s[wr * TA * 16 + i * 16 + (lane & 15)];
+#pragma unroll
+      for (int j = 0; j < TB; ++j) acc[i][j] = rs * acc[i][j] + acc2[i][j];
+    }
+    big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, nullptr);
+  } else {
+    big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane,
+                              (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
+  }
 }
 
 // LDS-ring kernels for the widest batched projections: RT x CT 16-row /
@@ -809,6 +843,15 @@ static hipError_t launch_big_ct(const GemmArgs &g, hipStream_t s, hipEvent_t ev0
 
 template <int EPI>
 static hipError_t launch_big(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if constexpr (EPI == EPI_QKV || EPI == EPI_GEGLU) {
+    if (g.A2) {  // the second accumulator: 128-column tiles keep the registers in bounds
+      if (!g.use_rstd) return hipErrorInvalidValue;
+      const size_t lds = (size_t)g.ssq_tiles * 128 * 4;
+      const int wgs = grid_tile_wgs(g.M, 16 * kBigRowTiles, g.N / (16 * 8));
+      UAD_LAUNCH((gemm_big_kernel<EPI, 8, true>), dim3(wgs), dim3(256), (uint32_t)lds, s, ev0, ev1, g);
+      return hipGetLastError();
+    }
+  }
   if constexpr (EPI == EPI_RESID_F32) {
     // Residual projections (N = d): 96-column tiles when they need fewer
     // 16 x 16 output tiles per CU than 128-column ones (1536 wide, 2048 rows:
@@ -830,9 +873,9 @@ static hipError_t launch_big(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, h
 // the projection shapes of the 1024- and 1536-wide experts (the rule picks
 // the faster kernel in 49 of 50 cases, the miss by 6%).
 static bool big_ok(int epi, const GemmArgs &g) {
-  const int ct = epi == EPI_GEGLU ? 16 : 8;
-  if (g.M < kBigM || g.N % (16 * ct) != 0 || g.A2 != nullptr || g.ssq_tiles > kMaxSsqTiles ||
-      (epi == EPI_QKV && g.q_dim % 16 != 0))
+  const int ct = (epi == EPI_GEGLU && !g.A2) ? 16 : 8;
+  if (g.M < kBigM || g.N % (16 * ct) != 0 || g.ssq_tiles > kMaxSsqTiles || (epi == EPI_QKV && g.q_dim % 16 != 0) ||
+      (g.A2 && epi != EPI_QKV && epi != EPI_GEGLU))
     return false;
   const int tiles = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles) * (g.N / (16 * ct));
   return tiles >= 90 && !(tiles < 128 && g.K > 4096);
@@ -840,8 +883,13 @@ static bool big_ok(int epi, const GemmArgs &g) {
 
 template <int EPI>
 static hipError_t big_attr() {
-  return hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, big_ct<EPI>()>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxSsqTiles * 128 * 4);
+  hipError_t e = hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, big_ct<EPI>()>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, kMaxSsqTiles * 128 * 4);
+  if constexpr (EPI == EPI_QKV || EPI == EPI_GEGLU)
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, 8, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              kMaxSsqTiles * 128 * 4);
+  return e;
 }
 
 hipError_t gemm_init() {
