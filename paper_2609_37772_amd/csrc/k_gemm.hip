@@ -67,7 +67,7 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
         const int KBd = g.d_model / kTileK;
         if (part == 1 || part == 4)
           store_op(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, j, KBd), mv);
-        else if (part == 0 && l == 0)
+        else if (part == 0 && l == 0 && g.next)
           store_op(g.next + afrag_index(row, j, KBd), g.h_in[(size_t)row * g.d_model + j] * (1.0f + mv));
       }
     }
@@ -576,7 +576,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
           const int part = r6 / g.d_model, jc = r6 - part * g.d_model;
           if (part == 1 || part == 4)
             st4h(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, jc, KBd), mv);
-          else if (part == 0 && l == 0)
+          else if (part == 0 && l == 0 && g.next)
             st4h(g.next + afrag_index(row, jc, KBd), ld4(g.h_in + (size_t)row * g.d_model + jc) * (mv + 1.0f));
         }
       }

@@ -73,13 +73,17 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
 // Adaptive-norm variant: te[m] = e(t_m) alone (K = d) as the time MLP's fp16
 // operand; the action token itself starts the residual stream,
 // h[m] = x_m W_in^T + b_in (fp32), with its per-16-column sums of squares.
+// t null: no time features (the schedule computed its time conditioning up
+// front); mod_a0 not null: also the first attention norm's operand
+// next = fp16(h_0 (1 + a)) with a the token's layer-0 scale, row stride mod_ld.
 template <int R>
 __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__ x, const float *__restrict__ t,
                                                         int M, int Da, int d, const float *__restrict__ w_in,
                                                         const float *__restrict__ b_in,
                                                         const float *__restrict__ freqs, op_t *__restrict__ te,
                                                         float *__restrict__ h, float *__restrict__ ssq,
-                                                        int m_alloc) {
+                                                        int m_alloc, const float *__restrict__ mod_a0, int mod_ld,
+                                                        op_t *__restrict__ next) {
   __shared__ float xs[R][64];
   const int m0 = blockIdx.x * R;
   const int rows = load_action_rows<R>(x, M, Da, xs);
@@ -105,10 +109,11 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
       float sq = acc[r] * acc[r];
       sq = sum_row16(sq);
       if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
+      if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]));
     }
   }
   const int half = d >> 1;
-  if (n < half)
+  if (t && n < half)
     for (int r = 0; r < rows; ++r) {
       const float arg = freqs[n] * t[m0 + r];
       store_op(te + afrag_index(m0 + r, n, KB), sinf(arg));
@@ -262,13 +267,41 @@ hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, con
 
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                            const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
-                           hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+                           hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, const float *mod_a0, int mod_ld,
+                           op_t *next) {
+  if (mod_a0 && !next) return hipErrorInvalidValue;
   if (M >= 1024)
     UAD_LAUNCH(temb_ada_kernel<16>, dim3((M + 15) / 16, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d,
-               w_in, b_in, freqs, te, h, ssq, m_alloc);
+               w_in, b_in, freqs, te, h, ssq, m_alloc, mod_a0, mod_ld, next);
   else
     UAD_LAUNCH(temb_ada_kernel<1>, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in, b_in,
-               freqs, te, h, ssq, m_alloc);
+               freqs, te, h, ssq, m_alloc, mod_a0, mod_ld, next);
+  return hipGetLastError();
+}
+
+// Time features of a whole schedule: row r = step * m_alloc + i takes the
+// flow time t[step * M + i] (i < M), padding rows time 0.
+__global__ __launch_bounds__(256) void time_feat_kernel(const float *__restrict__ t, int M, int m_alloc, int rows,
+                                                         int d, const float *__restrict__ freqs,
+                                                         op_t *__restrict__ te) {
+  const int r = blockIdx.x;
+  const int n = blockIdx.y * blockDim.x + threadIdx.x;
+  const int half = d >> 1;
+  if (r >= rows || n >= half) return;
+  const int st = r / m_alloc, i = r - st * m_alloc;
+  const float tv = i < M ? t[(size_t)st * M + i] : 0.f;
+  const float arg = freqs[n] * tv;
+  const int KB = d / kTileK;
+  store_op(te + afrag_index(r, n, KB), sinf(arg));
+  store_op(te + afrag_index(r, half + n, KB), cosf(arg));
+}
+
+hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps, int d, const float *freqs,
+                                op_t *te, hipStream_t s) {
+  if (M < 1 || m_alloc < M || m_alloc % 16 != 0 || n_steps < 1 || d % 64 != 0) return hipErrorInvalidValue;
+  const int rows = n_steps * m_alloc;
+  hipLaunchKernelGGL(time_feat_kernel, dim3(rows, (d / 2 + 255) / 256), dim3(256), 0, s, t, M, m_alloc, rows, d,
+                     freqs, te);
   return hipGetLastError();
 }
 

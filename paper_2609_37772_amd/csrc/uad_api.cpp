@@ -354,6 +354,7 @@ void uad_destroy(uad_ctx *c) {
   if (c->kcache) (void)hipFree(c->kcache);
   if (c->vtcache) (void)hipFree(c->vtcache);
   if (c->abuf) (void)hipFree(c->abuf);
+  if (c->pre_buf) (void)hipFree(c->pre_buf);
   for (auto &r : c->prof_pending) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
@@ -610,10 +611,18 @@ static uad_status check_step_args(uad_ctx *c, const void *x, const void *t, cons
 // attention (+ split-KV combine) -> O (+ residual, sums, next operand) ->
 // gate/up GeGLU (x rstd) -> down (+ residual, sums, next layer's operand)] ->
 // final norm/projection/Euler.
+// A step's slice of the schedule-level conditioning (modulations and shift
+// operands computed for every step up front), or per-step conditioning when null.
+struct AdaSlice {
+  const float *mod;        // [m_alloc][n_mod] rows of this step
+  const op_t *shift;       // layer 0's attention shift operand of this step
+  size_t shift_stride;     // elements from one [layer][norm] shift operand to the next
+};
+
 static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float *t, const float *dt,
                                const uint8_t *mask, const uint8_t *next_mask, int is_last, int step, float *v_out,
                                float *released, int32_t *release_step, int B, int H, float *vsum = nullptr,
-                               int vsum_tokens = 0) {
+                               int vsum_tokens = 0, const AdaSlice *pre = nullptr) {
   const int M = B * H, d = c->d, F = c->F;
   const size_t MA = c->m_alloc;
   hipError_t e = hipSuccess;
@@ -649,6 +658,11 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       g2.out = c->h; g2.ldo = d; g2.bias = c->t2_b; norm_fields(g2);
       g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n;
       UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_RESID_F32, g2, plan_gemm(EPI_RESID_F32, M, d, d), s, ea_, eb_));
+    } else if (pre) {
+      // conditioning computed for the whole schedule: h_0 = W_in x + b_in and the
+      // first attention norm's operand h_0 (1 + a) from this step's modulations
+      UAD_CHECK_CLS(K_TEMB, launch_temb_ada(x, nullptr, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs,
+                                            c->a_te, c->h, c->ssq, (int)MA, s, ea_, eb_, pre->mod, n_mod, c->a_n));
     } else {
       // adaptive norms: h_0 = W_in x + b_in, c = SiLU(W2 SiLU(W1 e(t) + b1) + b2), then every
       // modulation (a, b, g per norm site) in one GEMM whose epilogue also forms the
@@ -700,7 +714,10 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
       norm_fields(q); q.use_rstd = 1;
-      if (c->ada) q.A2 = c->mod_shift_ops + (size_t)(2 * l) * MA * d;
+      const float *mod_base = pre ? pre->mod : c->mod;
+      const op_t *shift_base = pre ? pre->shift : c->mod_shift_ops;
+      const size_t shift_stride = pre ? pre->shift_stride : MA * d;
+      if (c->ada) q.A2 = shift_base + (size_t)(2 * l) * shift_stride;
       UAD_CHECK_CLS(K_GEMM_QKV, launch_gemm(EPI_QKV, q, pq, s, ea_, eb_));
       at.kc = kc; at.vtc = vtc;
       at.pre_attn = Prefetch{};
@@ -725,21 +742,21 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       o.out = c->h; o.ldo = d; norm_fields(o);
       o.gain_next = lp.mlp_norm; o.next = c->a_n;
       if (c->ada) {
-        const float *ml = c->mod + (size_t)l * 6 * d;
+        const float *ml = mod_base + (size_t)l * 6 * d;
         o.mod_ld = n_mod; o.mod_gate = ml + 2 * d; o.mod_scale_next = ml + 3 * d; o.gain_next = nullptr;
       }
       UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, po, s, ea_, eb_));
       GemmArgs gu{};
       gu.M = M; gu.A = c->a_n; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
       gu.out = c->a_g; gu.ldo = F; norm_fields(gu); gu.use_rstd = 1;
-      if (c->ada) gu.A2 = c->mod_shift_ops + (size_t)(2 * l + 1) * MA * d;
+      if (c->ada) gu.A2 = shift_base + (size_t)(2 * l + 1) * shift_stride;
       UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU, gu, pg, s, ea_, eb_));
       GemmArgs dn{};
       dn.M = M; dn.A = c->a_g; dn.W = lp.wdown; dn.N = d; dn.K = F;
       dn.out = c->h; dn.ldo = d; norm_fields(dn);
       dn.gain_next = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr; dn.next = c->a_n;
       if (c->ada) {
-        const float *ml = c->mod + (size_t)l * 6 * d;
+        const float *ml = mod_base + (size_t)l * 6 * d;
         dn.mod_ld = n_mod; dn.mod_gate = ml + 5 * d; dn.gain_next = nullptr;
         dn.mod_scale_next = (l + 1 < c->L) ? ml + 6 * d : nullptr;
       }
@@ -753,10 +770,84 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
   f.debug_field = c->dbg ? 1 : 0; f.dbg_alpha = c->dbg_alpha; f.dbg_beta = c->dbg_beta;
   f.vsum = vsum; f.vsum_tokens = vsum_tokens; f.chunk = H;
   if (c->ada) {
-    f.mod_scale = c->mod + (size_t)c->L * 6 * d; f.mod_shift = f.mod_scale + d; f.mod_ld = c->n_mod;
+    f.mod_scale = (pre ? pre->mod : c->mod) + (size_t)c->L * 6 * d; f.mod_shift = f.mod_scale + d;
+    f.mod_ld = c->n_mod;
   }
   UAD_CHECK_CLS(K_FINAL, launch_final(f, s, ea_, eb_));
 #undef UAD_CHECK_CLS
+  return UAD_OK;
+}
+
+// Schedule-level conditioning applies to small batches (projections bound by
+// the weight stream, where the modulation matrix would be read once per step)
+// when the buffers for n_steps x m_alloc rows are in place.
+static bool ada_schedule_level(const uad_ctx *c, size_t M, int n_steps) {
+  return c->ada && !c->dbg && M <= 256 && (size_t)n_steps * c->m_alloc <= c->pre_rows;
+}
+
+// Grow the schedule-level conditioning buffers to `rows` rows (no-op when they
+// hold enough, or beyond a 2 GiB budget: the schedule then conditions per step).
+// Captured graphs reference the old buffers and are dropped.
+static void ensure_ada_rows(uad_ctx *c, size_t rows) {
+  if (rows <= c->pre_rows) return;
+  const size_t d = c->d;
+  Carve a;
+  const size_t o_te = a.take<uint16_t>(rows * d), o_z = a.take<uint16_t>(rows * d),
+               o_mod = a.take<float>(rows * c->n_mod), o_sh = a.take<uint16_t>((size_t)2 * c->L * rows * d);
+  if (a.off > ((size_t)2 << 30)) return;
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return;  // queued work may use the old buffers
+  for (auto &ge : c->graphs) (void)hipGraphExecDestroy(ge.exec);
+  c->graphs.clear();
+  if (c->pre_buf) (void)hipFree(c->pre_buf);
+  c->pre_buf = nullptr;
+  c->pre_rows = 0;
+  if (hipMalloc(&c->pre_buf, a.off) != hipSuccess) {
+    (void)hipGetLastError();
+    c->pre_buf = nullptr;
+    return;
+  }
+  char *b = (char *)c->pre_buf;
+  c->pre_te = (op_t *)(b + o_te);
+  c->pre_z = (op_t *)(b + o_z);
+  c->pre_mod = (float *)(b + o_mod);
+  c->pre_shift = (op_t *)(b + o_sh);
+  c->pre_rows = rows;
+}
+
+// The time conditioning of every step of a schedule: time features of its
+// n_steps x m_alloc rows, time MLP, and all modulations in one GEMM (the first
+// attention norm's operand needs h_0 and is formed per step).
+static uad_status enqueue_ada_schedule(uad_ctx *c, hipStream_t s, const GraphKey &k) {
+  const int d = c->d, rows = k.n_steps * (int)c->m_alloc;
+  const int M = k.B * k.H;
+  hipError_t e = hipSuccess;
+#define UAD_PRE_CLS(cls, call)                         \
+  do {                                                 \
+    hipEvent_t ea_ = nullptr, eb_ = nullptr;           \
+    if (c->prof_on) {                                  \
+      ea_ = pool_event(c);                             \
+      eb_ = pool_event(c);                             \
+    }                                                  \
+    e = (call);                                        \
+    if (e != hipSuccess) return hip_fail(c, e, #call); \
+    if (c->prof_on) c->prof_pending.push_back({cls, ea_, eb_}); \
+  } while (0)
+  e = launch_time_features(k.t, M, (int)c->m_alloc, k.n_steps, d, c->freqs, c->pre_te, s);
+  if (e != hipSuccess) return hip_fail(c, e, "launch_time_features");
+  GemmArgs g{};
+  g.M = rows; g.m_alloc = rows; g.A = c->pre_te; g.W = c->t1_w; g.N = d; g.K = d; g.out = c->pre_z; g.ldo = d;
+  g.bias = c->t1_b;
+  UAD_PRE_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, rows, d, d), s, ea_, eb_));
+  GemmArgs g2{};
+  g2.M = rows; g2.m_alloc = rows; g2.A = c->pre_z; g2.W = c->t2_w; g2.N = d; g2.K = d; g2.out = c->pre_te;
+  g2.ldo = d; g2.bias = c->t2_b;
+  UAD_PRE_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_SILU, g2, plan_gemm(EPI_BIAS_SILU, rows, d, d), s, ea_, eb_));
+  GemmArgs gm{};
+  gm.M = rows; gm.m_alloc = rows; gm.A = c->pre_te; gm.W = c->w_mod; gm.N = c->n_mod; gm.K = d; gm.out = c->pre_mod;
+  gm.ldo = c->n_mod; gm.bias = c->b_mod; gm.mod_shift_ops = c->pre_shift; gm.shift_stride = (size_t)rows * d;
+  gm.h_in = nullptr; gm.next = nullptr; gm.d_model = d; gm.n_layers = c->L;
+  UAD_PRE_CLS(K_GEMM_MOD, launch_gemm(EPI_MOD, gm, plan_gemm(EPI_MOD, rows, c->n_mod, d), s, ea_, eb_));
+#undef UAD_PRE_CLS
   return UAD_OK;
 }
 
@@ -767,11 +858,22 @@ static uad_status enqueue_schedule(uad_ctx *c, hipStream_t s, const GraphKey &k)
     hipError_t e = launch_stamp(k.step_ticks, s);
     if (e != hipSuccess) return hip_fail(c, e, "launch_stamp");
   }
+  const bool pre = ada_schedule_level(c, M, k.n_steps);
+  if (pre) {
+    uad_status rs = enqueue_ada_schedule(c, s, k);
+    if (rs != UAD_OK) return rs;
+  }
   for (int st = 0; st < k.n_steps; ++st) {
     const bool last = k.is_schedule ? st == k.n_steps - 1 : false;
     const uint8_t *next = (k.is_schedule && !last) ? k.mask + (st + 1) * M : nullptr;
+    AdaSlice sl{};
+    if (pre) {
+      sl.mod = c->pre_mod + (size_t)st * c->m_alloc * c->n_mod;
+      sl.shift = c->pre_shift + (size_t)st * c->m_alloc * c->d;
+      sl.shift_stride = (size_t)k.n_steps * c->m_alloc * c->d;
+    }
     uad_status rs = enqueue_step(c, s, k.x, k.t + st * M, k.dt + st * M, k.mask + st * M, next, last ? 1 : 0, st,
-                                 k.v_out, k.released, k.release_step, k.B, k.H);
+                                 k.v_out, k.released, k.release_step, k.B, k.H, nullptr, 0, pre ? &sl : nullptr);
     if (rs != UAD_OK) return rs;
     if (k.step_ticks) {
       hipError_t e = launch_stamp(k.step_ticks + st + 1, s);
@@ -794,14 +896,30 @@ static uad_status enqueue_release_phase(uad_ctx *c, hipStream_t s, const GraphKe
   a.dt_star = -(1.0f / (float)k.Nstar); a.reconcile = k.reconcile;
   hipError_t e = hipSuccess;
   const int st0 = k.kind == 1 ? 0 : k.Kr, st1 = k.kind == 1 ? k.Kr : k.Nstar;
+  // schedule-level conditioning: phase 1 computes it for all N* steps (the same
+  // rows, kernels and values as a uniform N*-step schedule), phase 2 reads it
+  const bool pre = ada_schedule_level(c, M, k.Nstar);
   if (k.kind == 1) {
     if (k.step_ticks && (e = launch_stamp(k.step_ticks, s)) != hipSuccess) return hip_fail(c, e, "launch_stamp");
     if ((e = launch_tr_init(a, s)) != hipSuccess) return hip_fail(c, e, "launch_tr_init");
+    if (pre) {
+      GraphKey kt = k;
+      kt.t = c->tr_t;
+      kt.n_steps = k.Nstar;
+      uad_status rs = enqueue_ada_schedule(c, s, kt);
+      if (rs != UAD_OK) return rs;
+    }
   }
   for (int st = st0; st < st1; ++st) {
+    AdaSlice sl{};
+    if (pre) {
+      sl.mod = c->pre_mod + (size_t)st * c->m_alloc * c->n_mod;
+      sl.shift = c->pre_shift + (size_t)st * c->m_alloc * c->d;
+      sl.shift_stride = (size_t)k.Nstar * c->m_alloc * c->d;
+    }
     uad_status rs = enqueue_step(c, s, k.x, c->tr_t + st * M, c->tr_dt + st * M, c->tr_mask + st * M, nullptr, 0, st,
                                  nullptr, nullptr, nullptr, k.B, k.H, k.kind == 1 && k.reconcile ? c->tr_vsum : nullptr,
-                                 k.U);
+                                 k.U, pre ? &sl : nullptr);
     if (rs != UAD_OK) return rs;
     if (k.step_ticks && (e = launch_stamp(k.step_ticks + st + 1, s)) != hipSuccess)
       return hip_fail(c, e, "launch_stamp");
@@ -886,6 +1004,7 @@ uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, cons
   if (st != UAD_OK) return st;
   if (n_steps < 1) return fail(c, UAD_E_INVALID, "uad_denoise_schedule: n_steps must be >= 1");
   (void)hipSetDevice(c->device);
+  if (c->ada && !c->dbg && (size_t)batch * chunk <= 256) ensure_ada_rows(c, (size_t)n_steps * c->m_alloc);
   GraphKey k{};
   k.kind = 0;
   k.is_schedule = true;
@@ -956,6 +1075,7 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
       host_dev = (float *)pa.devicePointer;
     (void)hipGetLastError();  // pageable memory: the query's error is expected
   }
+  if (c->ada && !c->dbg && M <= 256) ensure_ada_rows(c, (size_t)Nstar * c->m_alloc);
   GraphKey k{};
   k.kind = 1;
   k.x = x; k.B = batch; k.H = chunk; k.n_steps = Nstar; k.step_ticks = step_ticks;

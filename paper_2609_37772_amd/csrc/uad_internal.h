@@ -258,7 +258,11 @@ hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, con
 // per-16-column sums of squares ssq[d/16][m_alloc]
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                            const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
-                           hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                           hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
+                           const float *mod_a0 = nullptr, int mod_ld = 0, op_t *next = nullptr);
+// sinusoidal time features of n_steps x m_alloc rows (rows past M in a step: time 0)
+hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps, int d, const float *freqs,
+                                op_t *te, hipStream_t s);
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
 hipError_t launch_tr_init(const TrArgs &a, hipStream_t s);     // x0 <- x, vsum <- 0
@@ -351,6 +355,14 @@ struct uad_ctx {
   float *b_mod = nullptr;             // [n_mod]
   float *mod = nullptr;               // [m_alloc][n_mod] per token: per layer (a,b,g)_attn (a,b,g)_mlp, then (a,b)_final
   uad::op_t *mod_shift_ops = nullptr; // [L][2][m_alloc*d] shifts as fp16 operands
+  // schedule-level conditioning (small batches): the modulations depend on the
+  // flow time only, so a schedule computes them for all its steps at once,
+  // n_steps x m_alloc rows, and each step reads its slice
+  void *pre_buf = nullptr;
+  size_t pre_rows = 0;                // rows the buffers hold
+  float *pre_mod = nullptr;           // [rows][n_mod]
+  uad::op_t *pre_shift = nullptr;     // [L][2][rows*d] fragment order
+  uad::op_t *pre_te = nullptr, *pre_z = nullptr;  // [rows][d] time MLP operands
 
   // urgency-aware release with Trajectory Reconciliation
   float *tr_x0 = nullptr, *tr_vsum = nullptr;  // [m_alloc][Da]
