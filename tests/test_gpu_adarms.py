@@ -128,3 +128,37 @@ def test_adarms_batched_sampled_envs(gpu, batch):
         log(f"[pi05 B={batch}] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
         assert e <= VEL_RTOL and ea <= ACT_ATOL
     np.testing.assert_array_equal(rst.cpu().numpy(), O.release_steps(bud))
+
+
+@pytest.mark.parametrize("top", [64, 2])
+def test_adarms_schedule_level_conditioning_step_counts(gpu, top):
+    """The schedule computes the conditioning of all its steps at once: a
+    64-step schedule (a budget of 64, the largest the builder takes, on every
+    third token) and a 2-step one on the same context, which grow and reuse the
+    schedule-level buffers; both against the oracle, and a single joint step
+    afterwards still matches it."""
+    c = case("tiny_adarms")
+    H = c.wl.chunk
+    bud = np.full((1, H), top, np.int32)
+    bud[0, 1::3] = 1
+    r = O.denoise_schedule(c.oracle_model(), c.noise, bud)
+    n, tg, dtg, mg = c.expert.schedule_tables(bud)
+    assert n == top
+    x = dev(c.noise.astype(np.float32))
+    rel = torch.zeros_like(x)
+    rst = torch.full(bud.shape, -1, dtype=torch.int32, device="cuda")
+    c.expert.schedule(x, tg, dtg, mg, rel, rst)
+    torch.cuda.synchronize()
+    ex, er = np.abs(x.cpu().numpy() - r["x"]).max(), np.abs(rel.cpu().numpy() - r["released"]).max()
+    log(f"[tiny_adarms {top} steps] final max abs err {ex:.2e}, released {er:.2e}")
+    assert ex <= ACT_ATOL and er <= ACT_ATOL
+    np.testing.assert_array_equal(rst.cpu().numpy(), r["release_step"])
+    # one teacher-forced joint step at mid-schedule flow times
+    t = np.linspace(0.9, 0.1, H, dtype=np.float32)[None]
+    xg = dev(c.noise.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t), dev(np.zeros_like(t)), dev(np.zeros(t.shape, np.uint8)), vg)
+    torch.cuda.synchronize()
+    e = rel_err(vg.cpu().numpy(), O.velocity(c.oracle_model(), c.noise, t))
+    log(f"[tiny_adarms] single step after the schedule: velocity rel err {e:.2e}")
+    assert e <= VEL_RTOL
