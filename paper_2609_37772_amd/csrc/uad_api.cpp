@@ -790,6 +790,13 @@ static bool ada_schedule_level(const uad_ctx *c, size_t M, int n_steps) {
 // Captured graphs reference the old buffers and are dropped.
 static void ensure_ada_rows(uad_ctx *c, size_t rows) {
   if (rows <= c->pre_rows) return;
+  // a caller capturing the context stream into a graph of its own: no
+  // synchronisation or allocation now (the schedule conditions per step)
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(c->stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    (void)hipGetLastError();
+    return;
+  }
   const size_t d = c->d;
   Carve a;
   const size_t o_te = a.take<uint16_t>(rows * d), o_z = a.take<uint16_t>(rows * d),
