@@ -478,23 +478,25 @@ __device__ __forceinline__ void big_resid_rows(const GemmArgs &g, f32x4 (&acc)[T
   big_resid_store<NI, ADA, TA, TB>(g, acc, i0, mt, nt, lane, h0, gt, sc, has_next);
 }
 
-template <int EPI, int TA, int TB>
+template <int EPI, int TA, int TB, int I0 = 0, int NI = TA>
 __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA][TB], int mt, int nt, int lane,
                                              const float *rstd) {
   const int csub = 4 * (lane >> 4);
   if constexpr (EPI == EPI_RESID_F32) {
     if (g.mod_gate) {
 #pragma unroll
-      for (int i = 0; i < TA; ++i) big_resid_rows<1, true>(g, acc, i, mt, nt, lane);
+      for (int i = I0; i < I0 + NI; ++i) big_resid_rows<1, true>(g, acc, i, mt, nt, lane);
     } else {
-      // two halves: the whole tile's h0 at once would cost the main loop its second wave per SIMD
+      // the whole tile in two halves: all of its h0 at once would cost the
+      // main loop its second wave per SIMD (a half tile goes in one piece)
+      constexpr int HB = NI == TA ? TA / 2 : NI;
 #pragma unroll
-      for (int i = 0; i < TA; i += TA / 2) big_resid_rows<TA / 2, false>(g, acc, i, mt, nt, lane);
+      for (int i = I0; i < I0 + NI; i += HB) big_resid_rows<HB, false>(g, acc, i, mt, nt, lane);
     }
   } else if constexpr (EPI == EPI_QKV) {
     const int kvd = g.n_kv_heads * g.head_dim;
 #pragma unroll
-    for (int i = 0; i < TA; ++i) {
+    for (int i = I0; i < I0 + NI; ++i) {
       const int row = (mt + i) * 16 + (lane & 15);
       if (row >= g.M) continue;
       const float rs = rstd ? rstd[i * 16 + (lane & 15)] : 1.0f;
@@ -525,7 +527,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
   } else if constexpr (EPI == EPI_GEGLU) {
     const int KBo = g.ldo / kTileK;
 #pragma unroll
-    for (int i = 0; i < TA; ++i) {
+    for (int i = I0; i < I0 + NI; ++i) {
       const int row = (mt + i) * 16 + (lane & 15);
       if (row >= g.M) continue;
       const float rs = rstd ? rstd[i * 16 + (lane & 15)] : 1.0f;
@@ -543,7 +545,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
 #pragma unroll
     for (int j = 0; j < TB; ++j) bias[j] = ld4(g.bias + (nt + j) * 16 + csub);
 #pragma unroll
-    for (int i = 0; i < TA; ++i) {
+    for (int i = I0; i < I0 + NI; ++i) {
       const int row = (mt + i) * 16 + (lane & 15);
       if (row >= g.M) continue;
 #pragma unroll
@@ -562,7 +564,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
 #pragma unroll
     for (int j = 0; j < TB; ++j) bias[j] = ld4(g.bias + (nt + j) * 16 + csub);
 #pragma unroll
-    for (int i = 0; i < TA; ++i) {
+    for (int i = I0; i < I0 + NI; ++i) {
       const int row = (mt + i) * 16 + (lane & 15);
       if (row >= g.M) continue;
 #pragma unroll
@@ -587,23 +589,33 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
 // DUAL (adaptive norm, QKV / gate-up): a second accumulator takes A2 W (the
 // norm's shift through the weights) and is added after the rows' rstd has
 // scaled the first: rstd * (A W) + A2 W.
-template <int EPI, int CT, bool DUAL = false>
-__global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
+// KS = 2 (when the output tiles fill at most one round of CUs, so that a
+// 4-wave workgroup would leave each SIMD a single wave): 8 waves, waves
+// 4..7 take the odd k-blocks of the same tile; the two partial tiles are
+// summed through LDS and each k-half then runs the epilogue of half the
+// wave's row tiles.
+template <int EPI, int CT, bool DUAL = false, int KS = 1>
+__global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
   constexpr int TA = kBigRowTiles / 2, TB = CT / 2, PD = kBigPD;
   constexpr bool kRstd = (EPI == EPI_QKV || EPI == EPI_GEGLU);
   static_assert(!DUAL || kRstd, "the second operand belongs to a normalised projection");
+  static_assert(KS == 1 || (KS == 2 && !DUAL && TA % 2 == 0), "k-halves: single operand, even row tiles");
   typedef __attribute__((address_space(3))) void lds_void;
-  extern __shared__ float ssq_s[];  // [ssq_tiles][128] sums of squares of the workgroup's rows when kRstd
+  // [ssq_tiles][128] sums of squares of the workgroup's rows when kRstd;
+  // KS = 2: then the k-halves' exchange, [4 waves][2 halves][TA/2][TB][64] f32x4
+  extern __shared__ __align__(16) float ssq_s[];
   __shared__ float rstd_s[128];
   int mt0, nt0;
   if (!big_tile<CT>(g, mt0, nt0)) return;  // whole workgroup: padding of the grid
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wr = wave & 1, wc = wave >> 1;
+  const int wq = wave & 3, kh = wave >> 2;  // position in the 2 x 2 wave grid, k-half
+  const int wr = wq & 1, wc = wq >> 1;
   const int KB = g.K / kTileK;
+  const int nkb = KB / KS;  // this wave's k-blocks kh, kh + KS, ... (the host checks KB % KS == 0)
   const int mt_last = g.m_alloc / 16 - 1;  // allocated row tiles (rows >= M are computed, never stored)
   if (kRstd && g.use_rstd) {
     // this workgroup's 128 rows' per-tile sums of squares, straight to LDS
-    for (int j = wave; j < 2 * g.ssq_tiles; j += 4) {
+    for (int j = wave; j < 2 * g.ssq_tiles; j += 4 * KS) {
       const int tile = j >> 1, half = j & 1;
       const int row = min(mt0 * 16 + half * 64 + lane, g.M - 1);
       __builtin_amdgcn_global_load_lds((const void *)(g.ssq + (size_t)tile * g.m_alloc + row),
@@ -612,9 +624,11 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
   }
   const op_t *pa[TA], *pb[TB];
 #pragma unroll
-  for (int i = 0; i < TA; ++i) pa[i] = g.A + (size_t)min(mt0 + wr * TA + i, mt_last) * KB * kBlockElems + lane * 8;
+  for (int i = 0; i < TA; ++i)
+    pa[i] = g.A + ((size_t)min(mt0 + wr * TA + i, mt_last) * KB + kh) * kBlockElems + lane * 8;
 #pragma unroll
-  for (int j = 0; j < TB; ++j) pb[j] = g.W + (size_t)(nt0 + wc * TB + j) * KB * kBlockElems + lane * 8;
+  for (int j = 0; j < TB; ++j) pb[j] = g.W + ((size_t)(nt0 + wc * TB + j) * KB + kh) * kBlockElems + lane * 8;
+  constexpr size_t kStep = (size_t)KS * kBlockElems;  // between this wave's consecutive k-blocks
   constexpr int TA2 = DUAL ? TA : 1;
   const op_t *pa2[TA2];
 #pragma unroll
@@ -623,11 +637,11 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
   f16x8 ra[PD][TA], rb[PD][TB], ra2[PD][TA2];
 #pragma unroll
   for (int s = 0; s < PD; ++s) {
-    const int kb = min(s, KB - 1);
+    const int kb = min(s, nkb - 1);
 #pragma unroll
-    for (int i = 0; i < TA; ++i) ra[s][i] = *(const f16x8 *)(pa[i] + (size_t)kb * kBlockElems);
+    for (int i = 0; i < TA; ++i) ra[s][i] = *(const f16x8 *)(pa[i] + kb * kStep);
 #pragma unroll
-    for (int j = 0; j < TB; ++j) rb[s][j] = *(const f16x8 *)(pb[j] + (size_t)kb * kBlockElems);
+    for (int j = 0; j < TB; ++j) rb[s][j] = *(const f16x8 *)(pb[j] + kb * kStep);
     if constexpr (DUAL)
 #pragma unroll
       for (int i = 0; i < TA; ++i) ra2[s][i] = *(const f16x8 *)(pa2[i] + (size_t)kb * kBlockElems);
@@ -642,10 +656,10 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
     for (int i = 0; i < TA; ++i)
 #pragma unroll
       for (int j = 0; j < TB; ++j) acc2[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < KB; k0 += PD) {
+  for (int k0 = 0; k0 < nkb; k0 += PD) {
 #pragma unroll
     for (int s = 0; s < PD; ++s) {
-      if (k0 + s < KB) {
+      if (k0 + s < nkb) {
 #pragma unroll
         for (int i = 0; i < TA; ++i)
 #pragma unroll
@@ -655,11 +669,11 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
               acc2[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(rb[s][j], ra2[s][i], acc2[i][j], 0, 0, 0);
           }
       }
-      const int kb = min(k0 + s + PD, KB - 1);  // past the end: re-load the last block (never used)
+      const int kb = min(k0 + s + PD, nkb - 1);  // past the end: re-load the last block (never used)
 #pragma unroll
-      for (int i = 0; i < TA; ++i) ra[s][i] = *(const f16x8 *)(pa[i] + (size_t)kb * kBlockElems);
+      for (int i = 0; i < TA; ++i) ra[s][i] = *(const f16x8 *)(pa[i] + kb * kStep);
 #pragma unroll
-      for (int j = 0; j < TB; ++j) rb[s][j] = *(const f16x8 *)(pb[j] + (size_t)kb * kBlockElems);
+      for (int j = 0; j < TB; ++j) rb[s][j] = *(const f16x8 *)(pb[j] + kb * kStep);
       if constexpr (DUAL)
 #pragma unroll
         for (int i = 0; i < TA; ++i) ra2[s][i] = *(const f16x8 *)(pa2[i] + (size_t)kb * kBlockElems);
@@ -686,6 +700,39 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs g) {
       for (int j = 0; j < TB; ++j) acc[i][j] = rs * acc[i][j] + acc2[i][j];
     }
     big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, nullptr);
+  } else if constexpr (KS == 2) {
+    // Wave (wq, 0) keeps row tiles [0, H) and hands [H, TA) to wave (wq, 1),
+    // which keeps [H, TA); each adds the other's partial of what it keeps.
+    constexpr int H = TA / 2;
+    f32x4 *xch = (f32x4 *)(ssq_s + (kRstd && g.use_rstd ? g.ssq_tiles * 128 : 0));
+    f32x4 *mine = xch + (size_t)(wq * 2 + kh) * (H * TB * 64) + lane;
+    const f32x4 *other = xch + (size_t)(wq * 2 + (kh ^ 1)) * (H * TB * 64) + lane;
+    if (kh == 0) {
+#pragma unroll
+      for (int i = 0; i < H; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) mine[(i * TB + j) * 64] = acc[H + i][j];
+    } else {
+#pragma unroll
+      for (int i = 0; i < H; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) mine[(i * TB + j) * 64] = acc[i][j];
+    }
+    __syncthreads();
+    const float *rs = (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr;
+    if (kh == 0) {
+#pragma unroll
+      for (int i = 0; i < H; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = acc[i][j] + other[(i * TB + j) * 64];
+      big_epilogue<EPI, TA, TB, 0, H>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, rs);
+    } else {
+#pragma unroll
+      for (int i = 0; i < H; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[H + i][j] = other[(i * TB + j) * 64] + acc[H + i][j];
+      big_epilogue<EPI, TA, TB, H, H>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, rs);
+    }
   } else {
     big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane,
                               (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
@@ -832,11 +879,40 @@ constexpr int big_ct() { return EPI == EPI_GEGLU ? 16 : 8; }
 
 static int g_n_cu = 256;  // compute units of the device (set by gemm_init)
 
+// LDS of the k-halves' exchange (gemm_big_kernel with KS = 2)
+template <int CT>
+constexpr size_t big_xch_bytes() { return (size_t)4 * 2 * (kBigRowTiles / 4) * (CT / 2) * 64 * sizeof(f32x4); }
+
+// Whether a launch takes the k-halves (KS = 2): its tiles fill at most one
+// round of CUs (one 4-wave workgroup per CU would leave every SIMD a single
+// wave), K >= 1536 and the k-blocks split evenly.  Residual, QKV and
+// time-MLP-in epilogues only (128- or 96-column tiles, <= 256 registers at 8
+// waves).  Measured: the 1536-wide expert's QKV (2048 x 2048 x 1536, 256
+// tiles) 32.5 -> 25.5 us, its down 67.7 -> 65.2 us; the 1024-wide fleet's O
+// and down -2%; at K = 1024 (fleet time-MLP out) 18.8 -> 19.6 us, hence the
+// K bound.
+template <int EPI, int CT>
+static bool big_khalves(const GemmArgs &g) {
+  if constexpr (CT > 8 || !(EPI == EPI_RESID_F32 || EPI == EPI_QKV || EPI == EPI_BIAS_SILU)) {
+    return false;
+  } else {
+    const int tiles = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles) * (g.N / (16 * CT));
+    return tiles <= g_n_cu && g.K >= 1536 && (g.K / kTileK) % 2 == 0;
+  }
+}
+
 template <int EPI, int CT>
 static hipError_t launch_big_ct(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const bool rstd = (EPI == EPI_QKV || EPI == EPI_GEGLU) && g.use_rstd;
   const size_t lds = rstd ? (size_t)g.ssq_tiles * 128 * 4 : 0;
   const int wgs = grid_tile_wgs(g.M, 16 * kBigRowTiles, g.N / (16 * CT));
+  if constexpr (CT <= 8 && (EPI == EPI_RESID_F32 || EPI == EPI_QKV || EPI == EPI_BIAS_SILU)) {
+    if (big_khalves<EPI, CT>(g)) {
+      UAD_LAUNCH((gemm_big_kernel<EPI, CT, false, 2>), dim3(wgs), dim3(512), (uint32_t)(lds + big_xch_bytes<CT>()), s,
+                 ev0, ev1, g);
+      return hipGetLastError();
+    }
+  }
   UAD_LAUNCH((gemm_big_kernel<EPI, CT>), dim3(wgs), dim3(256), (uint32_t)lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
@@ -885,6 +961,17 @@ template <int EPI>
 static hipError_t big_attr() {
   hipError_t e = hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, big_ct<EPI>()>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, kMaxSsqTiles * 128 * 4);
+  if constexpr (EPI == EPI_RESID_F32 || EPI == EPI_QKV || EPI == EPI_BIAS_SILU) {
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, 8, false, 2>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)(kMaxSsqTiles * 128 * 4 + big_xch_bytes<8>()));
+    if constexpr (EPI == EPI_RESID_F32)
+      if (e == hipSuccess)
+        e = hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, 6, false, 2>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)(kMaxSsqTiles * 128 * 4 + big_xch_bytes<6>()));
+  }
   if constexpr (EPI == EPI_QKV || EPI == EPI_GEGLU)
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void *)gemm_big_kernel<EPI, 8, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
