@@ -748,18 +748,30 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
 // prologue (that wait is the prologue's own round trip) and folded into
 // rstd after the main loop.  Measured without epilogue (TFLOP/s):
 //   gate/up 256 x 128, 4 x 2 waves, 3 stages: 3200 x 8192 x 1024: 800 (vs
-//   711 register-streamed), 2048 x 12288 x 1536: 960 (vs 921);
+//   711 register-streamed), 2048 x 12288 x 1536: 960 (vs 921); with the
+//   GeGLU epilogue, 128 x 256 tiles (2 x 4 waves, same LDS per stage) beat
+//   256 x 128 in a same-box A/B: 73.3 -> 66.0 us and 89.3 -> 79.1 us (3200
+//   rows are 25 full 128-row panels instead of 12.5 of 256; 800 tiles
+//   instead of 832);
 //   QKV 128 x 128, 2 x 4 waves, 4 stages: 3200 x 2560 x 1024: 761 (vs 643;
 //   at 2048 x 2048 x 1536 the register-streamed kernel stays ahead, 651 vs 621).
+// Residual projections on the QKV shape (with epilogue, same-box A/B against
+// the 8-wave k-halves of the register-streamed kernel): 3200 x 1024 x 2048
+// 31.1 -> 29.0 us, x 4096 52.6 -> 48.9 us (2 x 4 waves; 4 x 2: 29.9 / 50.7);
+// the 1536-wide expert's (2048 rows, 96-column tiles there) lose 5%.
 constexpr int kRingNW = 8;
 template <int EPI>
 struct RingShape;
 template <>
 struct RingShape<EPI_GEGLU> {
-  static constexpr int RT = 16, CT = 8, WR = 4, WC = 2, NS = 3, MinM = 1024;
+  static constexpr int RT = 8, CT = 16, WR = 2, WC = 4, NS = 3, MinM = 1024;
 };
 template <>
 struct RingShape<EPI_QKV> {
+  static constexpr int RT = 8, CT = 8, WR = 2, WC = 4, NS = 4, MinM = 2560;
+};
+template <>
+struct RingShape<EPI_RESID_F32> {
   static constexpr int RT = 8, CT = 8, WR = 2, WC = 4, NS = 4, MinM = 2560;
 };
 
@@ -850,11 +862,25 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, g.use_rstd ? rstd_s + wr * TA * 16 : nullptr);
 }
 
+static int g_n_cu = 256;  // compute units of the device (set by gemm_init)
+
+// Residual projections: 96-column tiles of the register-streamed kernel when
+// they need fewer 16 x 16 output tiles per CU than 128-column ones (1536
+// wide, 2048 rows: 256 tiles of 48 instead of 192 tiles of 64 with 64 CUs
+// idle).
+static bool resid_prefers_96(const GemmArgs &g) {
+  auto per_cu = [&](int ct) {
+    const int tiles = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles) * (g.N / (16 * ct));
+    return (tiles + g_n_cu - 1) / g_n_cu * ct;
+  };
+  return g.N % 96 == 0 && per_cu(6) < per_cu(8);
+}
+
 template <int EPI>
 static bool ring_fits(const GemmArgs &g) {
   using S = RingShape<EPI>;
   return g.M >= S::MinM && g.N % (16 * S::CT) == 0 && g.A2 == nullptr && g.K / kTileK >= 1 &&
-         !(EPI == EPI_QKV && g.q_dim % 16 != 0);
+         !(EPI == EPI_QKV && g.q_dim % 16 != 0) && !(EPI == EPI_RESID_F32 && resid_prefers_96(g));
 }
 
 template <int EPI>
@@ -876,8 +902,6 @@ static hipError_t ring_attr() {
 // 16*CT columns per workgroup: 256 for gate/up (the widest projection), 128 otherwise
 template <int EPI>
 constexpr int big_ct() { return EPI == EPI_GEGLU ? 16 : 8; }
-
-static int g_n_cu = 256;  // compute units of the device (set by gemm_init)
 
 // LDS of the k-halves' exchange (gemm_big_kernel with KS = 2)
 template <int CT>
@@ -928,16 +952,8 @@ static hipError_t launch_big(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, h
       return hipGetLastError();
     }
   }
-  if constexpr (EPI == EPI_RESID_F32) {
-    // Residual projections (N = d): 96-column tiles when they need fewer
-    // 16 x 16 output tiles per CU than 128-column ones (1536 wide, 2048 rows:
-    // 256 tiles of 48 instead of 192 tiles of 64 with 64 CUs idle).
-    auto per_cu = [&](int ct) {
-      const int tiles = (g.M + 16 * kBigRowTiles - 1) / (16 * kBigRowTiles) * (g.N / (16 * ct));
-      return (tiles + g_n_cu - 1) / g_n_cu * ct;
-    };
-    if (g.N % 96 == 0 && per_cu(6) < per_cu(8)) return launch_big_ct<EPI, 6>(g, s, ev0, ev1);
-  }
+  if constexpr (EPI == EPI_RESID_F32)
+    if (resid_prefers_96(g)) return launch_big_ct<EPI, 6>(g, s, ev0, ev1);
   return launch_big_ct<EPI, big_ct<EPI>()>(g, s, ev0, ev1);
 }
 
@@ -986,6 +1002,7 @@ hipError_t gemm_init() {
   if (e == hipSuccess && g_n_cu < 1) e = hipErrorInvalidDevice;
   if (e == hipSuccess) e = ring_attr<EPI_GEGLU>();
   if (e == hipSuccess) e = ring_attr<EPI_QKV>();
+  if (e == hipSuccess) e = ring_attr<EPI_RESID_F32>();
   if (e == hipSuccess) e = big_attr<EPI_BIAS_SILU>();
   if (e == hipSuccess) e = big_attr<EPI_RESID_F32>();
   if (e == hipSuccess) e = big_attr<EPI_GEGLU>();
@@ -1038,6 +1055,7 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
   if (g.m_alloc < g.M || g.m_alloc % 16 != 0) return hipErrorInvalidValue;  // operand rows allocated
   if (epi == EPI_GEGLU && ring_fits<EPI_GEGLU>(g)) return launch_ring<EPI_GEGLU>(g, s, ev0, ev1);
   if (epi == EPI_QKV && ring_fits<EPI_QKV>(g)) return launch_ring<EPI_QKV>(g, s, ev0, ev1);
+  if (epi == EPI_RESID_F32 && ring_fits<EPI_RESID_F32>(g)) return launch_ring<EPI_RESID_F32>(g, s, ev0, ev1);
   if (big_ok(epi, g)) {
     switch (epi) {
       case EPI_BIAS_SILU: return launch_big<EPI_BIAS_SILU>(g, s, ev0, ev1);
