@@ -104,6 +104,24 @@ def test_fleet_sampled_envs(gpu):
     np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
 
 
+@pytest.mark.parametrize("batch", [48, 60])
+def test_fleet_ragged_row_panels(gpu, batch):
+    """Fleet model at 2400 / 3000 token rows, not a multiple of the batched
+    kernels' 128-row panels: the k-halves projections (2400 rows), the
+    residual LDS ring (3000 rows) and the 128 x 256 gate/up ring end on a
+    partial panel; the last environment's rows lie in it."""
+    c = make_case("pi0_fleet_b64", batch=batch)
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    _, v = gpu_velocity(c, c.noise, t[0], dt[0], mask[0])
+    for b in (0, batch - 1):
+        mb = c.oracle_model([b])
+        v_ref = O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0]
+        e = rel_err(v[b], v_ref)
+        log(f"[fleet B={batch}] env {b}: step-0 velocity rel err {e:.2e}")
+        assert e <= VEL_RTOL
+    c.expert.close()
+
+
 def test_large_sampled_envs(gpu):
     """24 layers, width 1536, GQA 12/2, H=128, B=16: sampled envs at two schedule steps."""
     c = case("large_b16")
