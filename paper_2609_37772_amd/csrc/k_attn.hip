@@ -214,18 +214,18 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
 #pragma unroll
           for (int h = 0; h < 2; ++h) s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[h][ks], qf[ks], s[h], 0, 0, 0);
       }
-      float mloc = -INFINITY;
+      // raw scores; keys past the end (last block only) masked to -inf; the
+      // scale (> 0) is applied to the block max and folded into exp2's FMA
+      if (k0 + 32 > a.n_keys) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = k0 + 16 * h + (lane >> 4) * 4 + r;
-          float v = s[h][r] * a.scale_log2;
-          if (key >= a.n_keys) v = -INFINITY;
-          s[h][r] = v;
-          mloc = fmaxf(mloc, v);
-        }
-      mloc = max_pair32(max_pair16(mloc));
+          for (int r = 0; r < 4; ++r)
+            if (k0 + 16 * h + (lane >> 4) * 4 + r >= a.n_keys) s[h][r] = -INFINITY;
+      }
+      float mloc = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+      mloc = max_pair32(max_pair16(mloc)) * a.scale_log2;
       // lazy rescale: raise the running max only past the threshold (whole wave)
       if (__any(mloc > m_run + kRescaleThreshold)) {
         const float m_new = fmaxf(m_run, mloc);
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[h][r] - m_run);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[h][r], a.scale_log2, -m_run));
           psum += p;
           pf[h * 4 + r] = (__bf16)p;
         }
