@@ -118,8 +118,15 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
 constexpr int kMaxTilesPerGroup = 4;
 constexpr int kMaxSsqTiles = 2048 / 16;  // d_model <= 2048
 
-template <int EPI, int T, int KPW, bool DUAL>
+static int g_n_cu = 256;  // compute units of the device (set by gemm_init)
+
+// PIPE (more than one pass, single operand): the operand registers are
+// double buffered, so the loads of pass p + 1 are in flight while the MFMAs
+// of pass p run and a launch pays one memory round trip instead of one per
+// pass.
+template <int EPI, int T, int KPW, bool DUAL, bool PIPE = false>
 __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
+  static_assert(!(PIPE && DUAL), "double-buffered passes: single operand only");
   extern __shared__ float red[];  // [waves][4*T*4 slots][64 lanes]
   constexpr bool kRstd = (EPI == EPI_QKV || EPI == EPI_GEGLU);
   __shared__ float ssq_s[kRstd ? kMaxSsqTiles : 1][64];  // this group's rows' per-tile sums of squares
@@ -146,7 +153,8 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
 
   // Operand loads of one pass (a run of KPW k-blocks per wave) and its MFMAs.
   f16x8 w[KPW][T], a[KPW][kMaxTilesPerGroup], a2[KPW][DUAL ? kMaxTilesPerGroup : 1];
-  auto load_pass = [&](int pass) {
+  f16x8 wb[PIPE ? KPW : 1][T], ab[PIPE ? KPW : 1][kMaxTilesPerGroup];  // PIPE: the second buffer
+  auto load_into = [&](int pass, auto &w, auto &a) {
     const int kb0 = (pass * waves + wave) * KPW;
     const op_t *wp = g.W + ((size_t)tile0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
@@ -160,7 +168,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       const bool ok = (m0 + mt * 16 + (lane & 15)) < g.M;
 #pragma unroll
       for (int j = 0; j < KPW; ++j) a[j][mt] = ok ? *(const f16x8 *)(ap + ((size_t)mt * KB + j) * kBlockElems) : f16x8{};
-      if (DUAL) {
+      if constexpr (DUAL) {
         const op_t *ap2 = g.A2 + ((size_t)mt0 * KB + kb0) * kBlockElems + lane * 8;
 #pragma unroll
         for (int j = 0; j < KPW; ++j)
@@ -168,7 +176,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       }
     }
   };
-  auto mma_pass = [&]() {
+  auto mma_from = [&](const auto &w, const auto &a) {
 #pragma unroll
     for (int mt = 0; mt < kMaxTilesPerGroup; ++mt) {
       if (mt >= nmt) break;
@@ -187,7 +195,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   // The first pass's operand loads go out first: any wait for the loads
   // issued after them (norm statistics, epilogue operands) covers them too,
   // so the kernel pays one memory round trip before its first MFMA.
-  load_pass(0);
+  load_into(0, w, a);
   // Every global load the kernel needs is issued before the first use so a
   // launch costs one memory round trip:
   //  * rstd of this group's rows comes from the residual GEMM's per-tile sums
@@ -228,9 +236,20 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
     }
   }
 
-  for (int pass = 0; pass < passes; ++pass) {
-    if (pass > 0) load_pass(pass);
-    mma_pass();
+  if constexpr (PIPE) {
+    for (int pass = 0; pass < passes; pass += 2) {
+      if (pass + 1 < passes) load_into(pass + 1, wb, ab);
+      mma_from(w, a);
+      if (pass + 1 < passes) {
+        if (pass + 2 < passes) load_into(pass + 2, w, a);
+        mma_from(wb, ab);
+      }
+    }
+  } else {
+    for (int pass = 0; pass < passes; ++pass) {
+      if (pass > 0) load_into(pass, w, a);
+      mma_from(w, a);
+    }
   }
 
   if (kRstd && g.use_rstd) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the LDS-direct sums landed
@@ -333,7 +352,14 @@ static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, 
       return hipGetLastError();
     }
   }
-  UAD_LAUNCH((gemm_kernel<EPI, T, KPW, false>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
+  // Double-buffered passes hold ~200 registers, one 8-wave workgroup per CU:
+  // only when the grid has no more workgroups than CUs (batch 1: down 4
+  // passes, O 2; step 0.700 -> 0.696 ms same-box; at 8 environments, 448
+  // workgroups, they lost 4% against two co-resident workgroups per CU).
+  if (p.passes > 1 && (long)grid.x * grid.z <= g_n_cu)
+    UAD_LAUNCH((gemm_kernel<EPI, T, KPW, false, true>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
+  else
+    UAD_LAUNCH((gemm_kernel<EPI, T, KPW, false>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
 
@@ -862,7 +888,6 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, g.use_rstd ? rstd_s + wr * TA * 16 : nullptr);
 }
 
-static int g_n_cu = 256;  // compute units of the device (set by gemm_init)
 
 // Residual projections: 96-column tiles of the register-streamed kernel when
 // they need fewer 16 x 16 output tiles per CU than 128-column ones (1536
