@@ -65,8 +65,10 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
   if (n < half)
     for (int r = 0; r < rows; ++r) {
       const float arg = freqs[n] * t[m0 + r];
-      store_op(te + afrag_index(m0 + r, d + n, KB), sinf(arg));
-      store_op(te + afrag_index(m0 + r, d + half + n, KB), cosf(arg));
+      float sv, cv;
+      sincosf(arg, &sv, &cv);  // one range reduction for both
+      store_op(te + afrag_index(m0 + r, d + n, KB), sv);
+      store_op(te + afrag_index(m0 + r, d + half + n, KB), cv);
     }
 }
 
@@ -116,8 +118,10 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
   if (t && n < half)
     for (int r = 0; r < rows; ++r) {
       const float arg = freqs[n] * t[m0 + r];
-      store_op(te + afrag_index(m0 + r, n, KB), sinf(arg));
-      store_op(te + afrag_index(m0 + r, half + n, KB), cosf(arg));
+      float sv, cv;
+      sincosf(arg, &sv, &cv);  // one range reduction for both
+      store_op(te + afrag_index(m0 + r, n, KB), sv);
+      store_op(te + afrag_index(m0 + r, half + n, KB), cv);
     }
 }
 
@@ -126,6 +130,25 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
 // Workgroup = (token m, group of up to 8 action dims); thread t owns columns
 // t + 256 i of the row for all 8 dims, loads unconditional as above.
 constexpr int kFinalOuts = 8;
+
+// Masked Euler update of token m, action dim a with velocity v (a copy when
+// frozen), the velocity outputs and the release bookkeeping.
+__device__ __forceinline__ void euler_out(const FinalArgs &f, int m, int a, float v) {
+  const size_t idx = (size_t)m * f.Da + a;
+  const float dtm = f.dt[m];
+  const bool frozen = (f.mask[m] != 0) || (dtm == 0.0f);
+  const float xo = f.x[idx];
+  const float xn = frozen ? xo : xo + dtm * v;
+  f.x[idx] = xn;
+  if (f.v_out) f.v_out[idx] = v;
+  if (f.vsum && (m % f.chunk) < f.vsum_tokens) f.vsum[idx] += v;
+  const bool releasing = !frozen && (f.is_last_step || (f.next_mask && f.next_mask[m] != 0));
+  if (releasing) {
+    if (f.released) f.released[idx] = xn;
+    if (f.release_step && a == 0) f.release_step[m] = f.step;
+  }
+}
+
 template <int NC>
 __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
   __shared__ float scratch[4];
@@ -178,22 +201,62 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
     }
   }
   __syncthreads();
-  if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da) {
-    const int a = a0 + threadIdx.x;
-    const size_t idx = (size_t)m * f.Da + a;
-    const float v = vs[threadIdx.x];
-    const float dtm = f.dt[m];
-    const bool frozen = (f.mask[m] != 0) || (dtm == 0.0f);
-    const float xo = f.x[idx];
-    const float xn = frozen ? xo : xo + dtm * v;
-    f.x[idx] = xn;
-    if (f.v_out) f.v_out[idx] = v;
-    if (f.vsum && (m % f.chunk) < f.vsum_tokens) f.vsum[idx] += v;
-    const bool releasing = !frozen && (f.is_last_step || (f.next_mask && f.next_mask[m] != 0));
-    if (releasing) {
-      if (f.released) f.released[idx] = xn;
-      if (f.release_step && a == 0) f.release_step[m] = f.step;
+  if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da) euler_out(f, m, a0 + threadIdx.x, vs[threadIdx.x]);
+}
+
+// Batched steps (many tokens, no adaptive norm, no debug field): R tokens per
+// workgroup share every W_out load (one W_out read per R tokens; one token
+// per workgroup read W_out 3200 times per step at 64 environments).
+template <int NC, int R>
+__global__ __launch_bounds__(256) void final_rows_kernel(FinalArgs f) {
+  __shared__ float red[4][R];
+  __shared__ float wsum[4][R][kFinalOuts];
+  const int m0 = blockIdx.x * R;
+  const int a0 = blockIdx.y * kFinalOuts;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int d = f.d;
+  float gv[NC], wv[kFinalOuts][NC], hv[R][NC];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const bool in = threadIdx.x + 256 * i < d;  // clamped duplicate columns contribute nothing
+    const int c = min(threadIdx.x + 256 * i, d - 1);
+    const float g = f.gain[c];
+    gv[i] = in ? g : 0.f;
+#pragma unroll
+    for (int o = 0; o < kFinalOuts; ++o) wv[o][i] = f.w_out[(size_t)min(a0 + o, f.Da - 1) * d + c];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float hh = f.h[(size_t)min(m0 + r, f.M - 1) * d + c];
+      hv[r][i] = in ? hh : 0.f;
     }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) ss += hv[r][i] * hv[r][i];
+    ss = sum_wave64(ss);
+    if (lane == 0) red[wave][r] = ss;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const float rstd = 1.0f / sqrtf(((red[0][r] + red[1][r]) + (red[2][r] + red[3][r])) / (float)d + f.eps);
+#pragma unroll
+    for (int o = 0; o < kFinalOuts; ++o) {
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < NC; ++i) acc += (hv[r][i] * rstd * gv[i]) * wv[o][i];
+      acc = sum_wave64(acc);
+      if (lane == 0) wsum[wave][r][o] = acc;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < R * kFinalOuts) {
+    const int r = threadIdx.x / kFinalOuts, o = threadIdx.x - r * kFinalOuts;
+    const int m = m0 + r, a = a0 + o;
+    if (m < f.M && a < f.Da)
+      euler_out(f, m, a, ((wsum[0][r][o] + wsum[1][r][o]) + (wsum[2][r][o] + wsum[3][r][o])) + f.b_out[a]);
   }
 }
 
@@ -292,8 +355,10 @@ __global__ __launch_bounds__(256) void time_feat_kernel(const float *__restrict_
   const float tv = i < M ? t[(size_t)st * M + i] : 0.f;
   const float arg = freqs[n] * tv;
   const int KB = d / kTileK;
-  store_op(te + afrag_index(r, n, KB), sinf(arg));
-  store_op(te + afrag_index(r, half + n, KB), cosf(arg));
+  float sv, cv;
+  sincosf(arg, &sv, &cv);  // one range reduction for both
+  store_op(te + afrag_index(r, n, KB), sv);
+  store_op(te + afrag_index(r, half + n, KB), cv);
 }
 
 hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps, int d, const float *freqs,
@@ -306,6 +371,16 @@ hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps,
 }
 
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if (f.M >= 1024 && !f.debug_field && !f.mod_scale) {
+    constexpr int R = 8;
+    const dim3 gr((f.M + R - 1) / R, (f.Da + kFinalOuts - 1) / kFinalOuts);
+    switch ((f.d + 255) / 256) {
+      case 4: UAD_LAUNCH((final_rows_kernel<4, R>), gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
+      case 6: UAD_LAUNCH((final_rows_kernel<6, R>), gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
+      case 8: UAD_LAUNCH((final_rows_kernel<8, R>), gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
+      default: break;  // other widths: one token per workgroup
+    }
+  }
   const dim3 grid(f.M, (f.Da + kFinalOuts - 1) / kFinalOuts);
   switch ((f.d + 255) / 256) {
     case 1: UAD_LAUNCH(final_kernel<1>, grid, dim3(256), 0, s, ev0, ev1, f); break;
