@@ -801,10 +801,10 @@ struct RingShape<EPI_RESID_F32> {
   static constexpr int RT = 8, CT = 8, WR = 2, WC = 4, NS = 4, MinM = 2560;
 };
 
-template <int EPI>
+template <int EPI, int NS = RingShape<EPI>::NS>
 __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   using S = RingShape<EPI>;
-  constexpr int RT = S::RT, CT = S::CT, WR = S::WR, WC = S::WC, NS = S::NS;
+  constexpr int RT = S::RT, CT = S::CT, WR = S::WR, WC = S::WC;
   constexpr int NBLK = RT + CT, LPW = NBLK / kRingNW;  // LDS-direct loads per wave per stage
   constexpr int TA = RT / WR, TB = CT / WC;            // 16 x 16 tiles per wave
   constexpr int ROWS = 16 * RT, TPR = 512 / ROWS;       // rows per workgroup, threads per row's statistics
@@ -908,20 +908,38 @@ static bool ring_fits(const GemmArgs &g) {
          !(EPI == EPI_QKV && g.q_dim % 16 != 0) && !(EPI == EPI_RESID_F32 && resid_prefers_96(g));
 }
 
-template <int EPI>
-static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+template <int EPI, int NS>
+static hipError_t launch_ring_ns(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   using S = RingShape<EPI>;
   const int wgs = grid_tile_wgs(g.M, 16 * S::RT, g.N / (16 * S::CT));
-  const uint32_t lds = (uint32_t)(S::NS * (S::RT + S::CT) * kBlockElems * sizeof(op_t));
-  UAD_LAUNCH((gemm_ring_kernel<EPI>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
+  const uint32_t lds = (uint32_t)(NS * (S::RT + S::CT) * kBlockElems * sizeof(op_t));
+  UAD_LAUNCH((gemm_ring_kernel<EPI, NS>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
   return hipGetLastError();
+}
+
+// Gate/up with K <= 1024 on a 2-stage ring (48 KiB of LDS, three workgroups
+// per CU): same-box A/B at 3200 x 8192 x 1024 68.6 -> 65.9 us; at K = 1536
+// (2048 x 12288) the 2-stage ring lost 84.2 -> 92.6 us, so 3 stages there.
+template <int EPI>
+static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if constexpr (EPI == EPI_GEGLU)
+    if (g.K <= 1024) return launch_ring_ns<EPI, 2>(g, s, ev0, ev1);
+  return launch_ring_ns<EPI, RingShape<EPI>::NS>(g, s, ev0, ev1);
+}
+
+template <int EPI, int NS>
+static hipError_t ring_attr_ns() {
+  using S = RingShape<EPI>;
+  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             NS * (S::RT + S::CT) * kBlockElems * (int)sizeof(op_t));
 }
 
 template <int EPI>
 static hipError_t ring_attr() {
-  using S = RingShape<EPI>;
-  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             S::NS * (S::RT + S::CT) * kBlockElems * (int)sizeof(op_t));
+  hipError_t e = ring_attr_ns<EPI, RingShape<EPI>::NS>();
+  if constexpr (EPI == EPI_GEGLU)
+    if (e == hipSuccess) e = ring_attr_ns<EPI, 2>();
+  return e;
 }
 
 // 16*CT columns per workgroup: 256 for gate/up (the widest projection), 128 otherwise
