@@ -304,6 +304,64 @@ def test_tr_reduces_tail_error_for_k_gt_1():
     assert e_tr < e_naive
 
 
+@pytest.mark.parametrize("K,Nstar,U", [(2, 6, 4), (3, 7, 5), (2, 3, 1)])
+def test_early_release_equals_per_token_schedule(K, Nstar, U):
+    """Sec. 4.2 Eq. 5: the urgent actions released after K steps of 1/K are
+    those of the per-token schedule with budgets K (urgent) and N* (tail),
+    built by the separately pinned table builder, bit for bit; without
+    reconciliation (plain UAER) the whole final state is that schedule's."""
+    m, *_ = tiny_model(dtype=np.float32, B=2)
+    H = 8
+    x0 = np.random.default_rng(31).standard_normal((2, H, 3)).astype(np.float32)
+    bud = np.full((2, H), Nstar)
+    bud[:, :U] = K
+    sch = O.denoise_schedule(m, x0, bud)
+    for reconcile in (True, False):
+        r = O.uad_tr_gac(m, x0, U=U, K=K, Nstar=Nstar, S=H, reconcile=reconcile)
+        assert r["released_urgent"].tobytes() == sch["released"][:, :U].tobytes()
+    r0 = O.uad_tr_gac(m, x0, U=U, K=K, Nstar=Nstar, S=H, reconcile=False)
+    assert r0["final"].tobytes() == sch["x"].tobytes()
+    assert r0["ghosts"] is None
+
+
+def _linear_flow(x, alpha, beta, dt, n):
+    """n Euler steps of size dt under v = alpha x + beta, closed form (float64)."""
+    g = (1.0 + alpha * dt) ** n
+    return g * x + (beta * (g - 1.0) / alpha if alpha != 0 else beta * n * dt)
+
+
+@pytest.mark.parametrize("K,Nstar", [(2, 5), (3, 7)])
+@pytest.mark.parametrize("alpha,beta", [(0.0, 0.6), (0.4, -0.3), (-1.1, 0.5)])
+def test_tr_linear_field_closed_form(K, Nstar, alpha, beta):
+    """Sec. 4.2 Eq. 5, Sec. 4.3 Eqs. 6-7, Sec. 4.4 Eqs. 8-9 under v = alpha x + beta.
+
+    Urgent tokens take K steps of dt_u = -1/K: a = g^K x_0 + beta (g^K - 1)/alpha
+    with g = 1 + alpha dt_u.  Their velocities are v_k = g^(k-1) (alpha x_0 + beta),
+    so TR gives x'_K = x_0 + dt* (alpha x_0 + beta) sum_{j<K} g^j, dt* = -1/N*;
+    the ghosts then take N* - K steps of dt*, the tail N* steps of dt*, and
+    GAC adds E / (S - U) with E = sum_i (ghost_i - a_i)."""
+    B, H, U, Da = 2, 9, 4, 3
+    x0 = np.random.default_rng(32).standard_normal((B, H, Da)).astype(np.float32)
+    fn = lambda x, t: (np.float32(alpha) * x + np.float32(beta)).astype(np.float32)
+    r = O.uad_tr_gac(None, x0, U=U, K=K, Nstar=Nstar, S=H, velocity_fn=fn)
+    x = x0.astype(np.float64)
+    du, ds = -1.0 / K, -1.0 / Nstar
+    a_ref = _linear_flow(x[:, :U], alpha, beta, du, K)
+    g = 1.0 + alpha * du
+    vsum = (alpha * x[:, :U] + beta) * sum(g ** j for j in range(K))
+    ghosts = _linear_flow(x[:, :U] + ds * vsum, alpha, beta, ds, Nstar - K)
+    tail = _linear_flow(x[:, U:], alpha, beta, ds, Nstar)
+    tol = dict(rtol=4e-6, atol=4e-6)
+    np.testing.assert_allclose(r["released_urgent"], a_ref, **tol)
+    np.testing.assert_allclose(r["ghosts"], ghosts, **tol)
+    np.testing.assert_allclose(r["final"][:, :U], ghosts, **tol)
+    np.testing.assert_allclose(r["final"][:, U:], tail, **tol)
+    E = np.sum(ghosts - a_ref, axis=1)
+    np.testing.assert_allclose(r["E"], E, rtol=2e-5, atol=2e-5)
+    np.testing.assert_allclose(r["executed"][:, :U], a_ref, **tol)
+    np.testing.assert_allclose(r["executed"][:, U:], tail + E[:, None, :] / (H - U), rtol=2e-5, atol=2e-5)
+
+
 def test_gac_closed_form():
     rng = np.random.default_rng(15)
     B, U, S, Da = 2, 3, 10, 4
