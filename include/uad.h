@@ -22,6 +22,20 @@
  *    Flow time runs from t = 1 (noise) to t = 0; the Euler step is
  *    x <- x + dt * v with dt = -1/N_i for an action with budget N_i.
  *  - A context is not thread-safe; use one per host thread.
+ *  - Errors of enqueued device work are reported by uad_synchronize: a
+ *    device status word collects them while the work runs.
+ *
+ * Where this interface differs from the bare statement of the problem (the
+ * four calls load_weights / set_prefix_kv / denoise_step / denoise_schedule):
+ *  - uad_denoise_schedule reports device wall-clock ticks (step_ticks, n_steps
+ *    + 1 entries, with uad_tick_rate_hz) instead of host nanoseconds per step,
+ *    because only the device can stamp the end of a step without a sync;
+ *  - uad_set_prefix_kv takes a dtype, so an fp32 prefix can be handed over
+ *    without a host-side bf16 conversion;
+ *  - uad_build_schedule takes max_steps, the capacity of the caller's tables;
+ *  - UAD_E_UNSUPPORTED and UAD_E_RANGE are added: the first for model
+ *    dimensions the kernels cannot tile, the second for fp16 operand overflow
+ *    found while the work ran.
  *  - Weights are named tensors in PyTorch Linear layout [out][in], row-major:
  *      action_in.w [d][Da], action_in.b [d],
  *      time_mlp_in.w [d][2d], time_mlp_in.b [d],
@@ -69,7 +83,8 @@ typedef enum {
   UAD_E_MISSING = 4,     /* a required weight tensor is absent or duplicated */
   UAD_E_HIP = 5,         /* a HIP runtime call failed (message has hipGetErrorString) */
   UAD_E_OOM = 6,         /* device allocation failed */
-  UAD_E_UNSUPPORTED = 7  /* model dimensions the kernels do not support */
+  UAD_E_UNSUPPORTED = 7, /* model dimensions the kernels do not support */
+  UAD_E_RANGE = 8        /* (from uad_synchronize) an fp16 operand of the enqueued work was not finite */
 } uad_status;
 
 enum { UAD_DTYPE_F32 = 0, UAD_DTYPE_BF16 = 1 };
@@ -102,7 +117,9 @@ typedef struct {
 } uad_tensor;
 
 /* Create a context on HIP device `device`.  `hip_stream` is a hipStream_t on
- * that device, or NULL to let the library create its own.  Allocates the
+ * that device, or NULL to let the library create its own; the work of a
+ * library-owned stream is ordered after what the caller queued on the null
+ * stream before each call, and the null stream's later work after it.  Allocates the
  * weight store, the prefix/chunk K/V store and all activation workspace for
  * the configured maxima.  Errors: UAD_E_INVALID (null/negative fields),
  * UAD_E_UNSUPPORTED (dimension the kernels cannot tile), UAD_E_OOM, UAD_E_HIP.
@@ -128,7 +145,8 @@ uad_status uad_set_stream(uad_ctx *ctx, void *hip_stream);
  * subnormal (absolute error <= 2^-25).  Norm gains, biases and the action
  * in/out projections are kept in fp32.  The data are COPIED into
  * library-owned device memory in the kernels' packed layout; the caller may
- * free its buffers on return.  Synchronous.  Errors: UAD_E_MISSING (absent or
+ * free its buffers on return.  Synchronous: waits for the context's queued
+ * work first, which may still read the weights being replaced.  Errors: UAD_E_MISSING (absent or
  * duplicated name, named in the message), UAD_E_SHAPE, UAD_E_INVALID (bad
  * dtype, or a projection weight that is NaN or beyond +-65504), UAD_E_HIP. */
 uad_status uad_load_weights(uad_ctx *ctx, const uad_tensor *tensors, int32_t n_tensors);
@@ -139,7 +157,8 @@ uad_status uad_load_weights(uad_ctx *ctx, const uad_tensor *tensors, int32_t n_t
  * [L][batch][P][Hkv][hd] arrays of `dtype` (F32 rounded to bf16, nearest-even),
  * host memory (on_device = 0) or device memory (on_device = 1).  COPIED into
  * the library's K/V store, where each step appends the chunk's own keys and
- * values after the prefix.  Synchronous.  Errors: UAD_E_INVALID,
+ * values after the prefix.  Synchronous: waits for the context's queued work
+ * first, which may still read the K/V being replaced.  Errors: UAD_E_INVALID,
  * UAD_E_SHAPE (batch > max_batch, P > max_prefix), UAD_E_HIP. */
 uad_status uad_set_prefix_kv(uad_ctx *ctx, const void *k, const void *v, int32_t dtype,
                              int32_t batch, int32_t prefix_len, int32_t on_device);
@@ -240,7 +259,11 @@ uad_status uad_build_schedule(const int32_t *budgets, int32_t batch, int32_t chu
  * action j measured from the request.  Pure host code. */
 uad_status uad_aal(const double *release, int32_t n, double t_act, double *aal_out);
 
-/* Block the host until all work enqueued on the context's stream is done. */
+/* Block the host until all work enqueued on the context's stream is done,
+ * then read and clear the context's device status word: UAD_E_RANGE when a
+ * GEMM or attention operand rounded to fp16 was not finite (|value| > 65504,
+ * or NaN) since the last call, UAD_E_HIP when an in-kernel wait gave up; the
+ * results of that work are then invalid.  Errors: UAD_E_HIP, UAD_E_RANGE. */
 uad_status uad_synchronize(uad_ctx *ctx);
 
 /* Device wall-clock tick rate (Hz) of the counter written to step_ticks. */

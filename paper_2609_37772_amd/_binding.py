@@ -28,7 +28,7 @@ UAD_DTYPE_F32, UAD_DTYPE_BF16 = 0, 1
 UAD_RELEASE_UAER, UAD_RELEASE_TR = 0, 1
 UAD_FLAG_ADARMS = 1
 STATUS_NAMES = {0: "UAD_OK", 1: "UAD_E_INVALID", 2: "UAD_E_SHAPE", 3: "UAD_E_STATE", 4: "UAD_E_MISSING",
-                5: "UAD_E_HIP", 6: "UAD_E_OOM", 7: "UAD_E_UNSUPPORTED"}
+                5: "UAD_E_HIP", 6: "UAD_E_OOM", 7: "UAD_E_UNSUPPORTED", 8: "UAD_E_RANGE"}
 EXPORTED_SYMBOLS = [
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
     "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_denoise_release",

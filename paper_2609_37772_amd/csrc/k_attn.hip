@@ -292,7 +292,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
       const float inv = 1.0f / lr[r];
 #pragma unroll
       for (int nt = 0; nt < NTO; ++nt)
-        store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv);
+        store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv, a.status);
     }
   } else {
     // Partials o_s / l_s in fp16 (bounded by max |V|), in the accumulator's
@@ -305,8 +305,9 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
     for (int r = 0; r < 4; ++r) inv[r] = 1.0f / lr[r];
 #pragma unroll
     for (int nt = 0; nt < NTO; ++nt) {
-      *(f16x4 *)(op + nt * 256) = f16x4{(op_t)(o[nt][0] * inv[0]), (op_t)(o[nt][1] * inv[1]),
-                                         (op_t)(o[nt][2] * inv[2]), (op_t)(o[nt][3] * inv[3])};
+      const float p0 = o[nt][0] * inv[0], p1 = o[nt][1] * inv[1], p2 = o[nt][2] * inv[2], p3 = o[nt][3] * inv[3];
+      *(f16x4 *)(op + nt * 256) = f16x4{(op_t)p0, (op_t)p1, (op_t)p2, (op_t)p3};
+      check_op4(p0, p1, p2, p3, a.status);
     }
     // lanes 0..15 hold the statistics of their own query row r0 + lane
     if (lane < 16) *(float2 *)(a.mlpart + (tile * 16 + lane) * 2) = float2{m_run, l_tot};
@@ -365,7 +366,8 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
     if (row >= a.rows) continue;
     const int hg = row / a.chunk, tok = row - hg * a.chunk;
     const int head = g * a.group + hg;
-    store_op(a.o + afrag_index(b * a.chunk + tok, head * hd + nt * 16 + (lane & 15), a.ldo / kTileK), num / den);
+    store_op(a.o + afrag_index(b * a.chunk + tok, head * hd + nt * 16 + (lane & 15), a.ldo / kTileK), num / den,
+             a.status);
   }
 }
 

@@ -66,9 +66,9 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
         const int part = r6 / g.d_model, j = r6 - part * g.d_model;
         const int KBd = g.d_model / kTileK;
         if (part == 1 || part == 4)
-          store_op(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, j, KBd), mv);
+          store_op(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, j, KBd), mv, g.status);
         else if (part == 0 && l == 0 && g.next)
-          store_op(g.next + afrag_index(row, j, KBd), g.h_in[(size_t)row * g.d_model + j] * (1.0f + mv));
+          store_op(g.next + afrag_index(row, j, KBd), g.h_in[(size_t)row * g.d_model + j] * (1.0f + mv), g.status);
       }
     }
   } else if (EPI == EPI_RESID_F32) {
@@ -82,16 +82,16 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
     sq = sum_row16(sq);
     if (row_ok) {
       if ((ln & 15) == 0) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
-      if (g.mod_scale_next || g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * sc);
+      if (g.mod_scale_next || g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * sc, g.status);
     }
   } else if (row_ok) {
     if (EPI == EPI_GEGLU) {
       const int col = (tile >> 1) * 16 + (ln & 15);
-      store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), gelu_tanh(v * rs) * (u * rs));
+      store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), gelu_tanh(v * rs) * (u * rs), g.status);
     } else {
       const int col = tile * 16 + (ln & 15);
       if (EPI == EPI_BIAS_SILU) {
-        store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), silu(v + g.bias[col]));
+        store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), silu(v + g.bias[col]), g.status);
       } else if (EPI == EPI_QKV) {
         v *= rs;
         if (col < g.q_dim) {
@@ -422,8 +422,9 @@ __device__ __forceinline__ bool big_tile(const GemmArgs &g, int &mt0, int &nt0) 
 // TA*16 rows.
 __device__ __forceinline__ f32x4 ld4(const float *p) { return *(const f32x4 *)p; }
 __device__ __forceinline__ void st4(float *p, f32x4 v) { *(f32x4 *)p = v; }
-__device__ __forceinline__ void st4h(op_t *p, f32x4 v) {
+__device__ __forceinline__ void st4h(op_t *p, f32x4 v, unsigned *status) {
   *(f16x4 *)p = f16x4{(op_t)v[0], (op_t)v[1], (op_t)v[2], (op_t)v[3]};
+  check_op4(v[0], v[1], v[2], v[3], status);
 }
 
 // Residual epilogue, store half, over NI row tiles starting at i0: h = h0 (or
@@ -451,7 +452,7 @@ __device__ __forceinline__ void big_resid_store(const GemmArgs &g, const f32x4 (
       sq = sum_pair32(sum_pair16(sq));  // the 4 lanes holding this row's 16 columns
       if (row_ok) {
         if (lane < 16) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
-        if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ADA ? ii : 0][j]);
+        if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ADA ? ii : 0][j], g.status);
       }
     }
   }
@@ -562,7 +563,8 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
         const int col = ((nt + j) >> 1) * 16 + csub;
         const f32x4 a = acc[i][j] * rs, u = acc[i][j + 1] * rs;
         st4h((op_t *)g.out + afrag_index(row, col, KBo),
-             f32x4{gelu_tanh(a[0]) * u[0], gelu_tanh(a[1]) * u[1], gelu_tanh(a[2]) * u[2], gelu_tanh(a[3]) * u[3]});
+             f32x4{gelu_tanh(a[0]) * u[0], gelu_tanh(a[1]) * u[1], gelu_tanh(a[2]) * u[2], gelu_tanh(a[3]) * u[3]},
+             g.status);
       }
     }
   } else if constexpr (EPI == EPI_BIAS_SILU) {
@@ -578,7 +580,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
       for (int j = 0; j < TB; ++j) {
         const f32x4 z = acc[i][j] + bias[j];
         st4h((op_t *)g.out + afrag_index(row, (nt + j) * 16 + csub, KBo),
-             f32x4{silu(z[0]), silu(z[1]), silu(z[2]), silu(z[3])});
+             f32x4{silu(z[0]), silu(z[1]), silu(z[2]), silu(z[3])}, g.status);
       }
     }
   } else if constexpr (EPI == EPI_MOD) {
@@ -603,9 +605,11 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
           const int r6 = col - l * per_layer;
           const int part = r6 / g.d_model, jc = r6 - part * g.d_model;
           if (part == 1 || part == 4)
-            st4h(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, jc, KBd), mv);
+            st4h(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, jc, KBd), mv,
+                 g.status);
           else if (part == 0 && l == 0 && g.next)
-            st4h(g.next + afrag_index(row, jc, KBd), ld4(g.h_in + (size_t)row * g.d_model + jc) * (mv + 1.0f));
+            st4h(g.next + afrag_index(row, jc, KBd), ld4(g.h_in + (size_t)row * g.d_model + jc) * (mv + 1.0f),
+                 g.status);
         }
       }
     }

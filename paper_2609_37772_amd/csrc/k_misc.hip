@@ -40,7 +40,8 @@ template <int R>
 __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, const float *__restrict__ t, int M,
                                                     int Da, int d, const float *__restrict__ w_in,
                                                     const float *__restrict__ b_in,
-                                                    const float *__restrict__ freqs, op_t *__restrict__ te) {
+                                                    const float *__restrict__ freqs, op_t *__restrict__ te,
+                                                    unsigned *status) {
   __shared__ float xs[R][64];
   const int m0 = blockIdx.x * R;
   const int rows = load_action_rows<R>(x, M, Da, xs);
@@ -59,7 +60,7 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
     }
 #pragma unroll
     for (int r = 0; r < R; ++r)
-      if (r < rows) store_op(te + afrag_index(m0 + r, n, KB), acc[r]);
+      if (r < rows) store_op(te + afrag_index(m0 + r, n, KB), acc[r], status);
   }
   const int half = d >> 1;
   if (n < half)
@@ -67,8 +68,8 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
       const float arg = freqs[n] * t[m0 + r];
       float sv, cv;
       sincosf(arg, &sv, &cv);  // one range reduction for both
-      store_op(te + afrag_index(m0 + r, d + n, KB), sv);
-      store_op(te + afrag_index(m0 + r, d + half + n, KB), cv);
+      store_op(te + afrag_index(m0 + r, d + n, KB), sv, status);
+      store_op(te + afrag_index(m0 + r, d + half + n, KB), cv, status);
     }
 }
 
@@ -85,7 +86,7 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
                                                         const float *__restrict__ freqs, op_t *__restrict__ te,
                                                         float *__restrict__ h, float *__restrict__ ssq,
                                                         int m_alloc, const float *__restrict__ mod_a0, int mod_ld,
-                                                        op_t *__restrict__ next) {
+                                                        op_t *__restrict__ next, unsigned *status) {
   __shared__ float xs[R][64];
   const int m0 = blockIdx.x * R;
   const int rows = load_action_rows<R>(x, M, Da, xs);
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
       float sq = acc[r] * acc[r];
       sq = sum_row16(sq);
       if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
-      if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]));
+      if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]), status);
     }
   }
   const int half = d >> 1;
@@ -120,8 +121,8 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
       const float arg = freqs[n] * t[m0 + r];
       float sv, cv;
       sincosf(arg, &sv, &cv);  // one range reduction for both
-      store_op(te + afrag_index(m0 + r, n, KB), sv);
-      store_op(te + afrag_index(m0 + r, half + n, KB), cv);
+      store_op(te + afrag_index(m0 + r, n, KB), sv, status);
+      store_op(te + afrag_index(m0 + r, half + n, KB), cv, status);
     }
 }
 
@@ -317,28 +318,28 @@ __global__ void stamp_kernel(uint64_t *dst) {
 }
 
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
-                       const float *b_in, const float *freqs, op_t *te, hipStream_t s,
+                       const float *b_in, const float *freqs, op_t *te, unsigned *status, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
   if (M >= 1024)
     UAD_LAUNCH(temb_kernel<16>, dim3((M + 15) / 16, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in,
-               b_in, freqs, te);
+               b_in, freqs, te, status);
   else
     UAD_LAUNCH(temb_kernel<1>, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in, b_in, freqs,
-               te);
+               te, status);
   return hipGetLastError();
 }
 
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                            const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
-                           hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, const float *mod_a0, int mod_ld,
-                           op_t *next) {
+                           unsigned *status, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, const float *mod_a0,
+                           int mod_ld, op_t *next) {
   if (mod_a0 && !next) return hipErrorInvalidValue;
   if (M >= 1024)
     UAD_LAUNCH(temb_ada_kernel<16>, dim3((M + 15) / 16, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d,
-               w_in, b_in, freqs, te, h, ssq, m_alloc, mod_a0, mod_ld, next);
+               w_in, b_in, freqs, te, h, ssq, m_alloc, mod_a0, mod_ld, next, status);
   else
     UAD_LAUNCH(temb_ada_kernel<1>, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in, b_in,
-               freqs, te, h, ssq, m_alloc, mod_a0, mod_ld, next);
+               freqs, te, h, ssq, m_alloc, mod_a0, mod_ld, next, status);
   return hipGetLastError();
 }
 
@@ -346,7 +347,7 @@ hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d,
 // flow time t[step * M + i] (i < M), padding rows time 0.
 __global__ __launch_bounds__(256) void time_feat_kernel(const float *__restrict__ t, int M, int m_alloc, int rows,
                                                          int d, const float *__restrict__ freqs,
-                                                         op_t *__restrict__ te) {
+                                                         op_t *__restrict__ te, unsigned *status) {
   const int r = blockIdx.x;
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
   const int half = d >> 1;
@@ -357,16 +358,16 @@ __global__ __launch_bounds__(256) void time_feat_kernel(const float *__restrict_
   const int KB = d / kTileK;
   float sv, cv;
   sincosf(arg, &sv, &cv);  // one range reduction for both
-  store_op(te + afrag_index(r, n, KB), sv);
-  store_op(te + afrag_index(r, half + n, KB), cv);
+  store_op(te + afrag_index(r, n, KB), sv, status);
+  store_op(te + afrag_index(r, half + n, KB), cv, status);
 }
 
 hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps, int d, const float *freqs,
-                                op_t *te, hipStream_t s) {
+                                op_t *te, unsigned *status, hipStream_t s) {
   if (M < 1 || m_alloc < M || m_alloc % 16 != 0 || n_steps < 1 || d % 64 != 0) return hipErrorInvalidValue;
   const int rows = n_steps * m_alloc;
   hipLaunchKernelGGL(time_feat_kernel, dim3(rows, (d / 2 + 255) / 256), dim3(256), 0, s, t, M, m_alloc, rows, d,
-                     freqs, te);
+                     freqs, te, status);
   return hipGetLastError();
 }
 

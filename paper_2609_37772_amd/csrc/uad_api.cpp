@@ -124,10 +124,9 @@ hipEvent_t pool_event(uad_ctx *c) {
   return e;
 }
 
-int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) {
+int attn_splits_nb(const uad_ctx *c, int B, int H, int n_blocks, int *bps) {
   const int rows = (c->Hq / c->Hkv) * H;
   const int qblocks = (rows + 63) / 64;
-  const int n_blocks = (P + H + 31) / 32;
   const int wgs = qblocks * B * c->Hkv;
   // Split the keys so that the query blocks x splits fill about one round of
   // workgroups (256 CUs): one chunk (one memory round trip) per split when
@@ -145,6 +144,34 @@ int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) {
   if (per > n_blocks) per = n_blocks;
   *bps = per;
   return (n_blocks + per - 1) / per;
+}
+
+int attn_splits(const uad_ctx *c, int B, int H, int P, int *bps) { return attn_splits_nb(c, B, H, (P + H + 31) / 32, bps); }
+
+// Split-KV partial rows (x head_dim) that a call with B environments, chunk H
+// and prefix P writes.
+size_t attn_part_rows(const uad_ctx *c, int B, int H, int P) {
+  int bps;
+  const int sp = attn_splits(c, B, H, P, &bps);
+  if (sp <= 1) return 0;
+  const size_t rows_pad = (size_t)((c->Hq / c->Hkv) * H + 63) / 64 * 64;
+  return (size_t)sp * B * c->Hkv * rows_pad;
+}
+
+// Work of a context that owns its stream is ordered after everything the
+// caller queued on the null stream before the call, and the null stream's
+// later work after it (a caller-provided stream orders itself).
+hipError_t order_before(uad_ctx *c) {
+  if (!c->own_stream) return hipSuccess;
+  hipError_t e = hipEventRecord(c->ev_in, nullptr);
+  if (e == hipSuccess) e = hipStreamWaitEvent(c->stream, c->ev_in, 0);
+  return e;
+}
+hipError_t order_after(uad_ctx *c) {
+  if (!c->own_stream) return hipSuccess;
+  hipError_t e = hipEventRecord(c->ev_out, c->stream);
+  if (e == hipSuccess) e = hipStreamWaitEvent(nullptr, c->ev_out, 0);
+  return e;
 }
 
 }  // namespace
@@ -179,7 +206,10 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->cfg = m;
   c->device = device;
   e = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device);
-  if (e != hipSuccess) return cerr(UAD_E_HIP, std::string("hipDeviceGetAttribute: ") + hipGetErrorString(e));
+  if (e != hipSuccess) {
+    delete c;
+    return cerr(UAD_E_HIP, std::string("hipDeviceGetAttribute: ") + hipGetErrorString(e));
+  }
   c->d = m.d_model;
   c->L = m.n_layers;
   c->Hq = m.n_heads;
@@ -280,16 +310,20 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   }
 
   // activation workspace (rows padded to 64 and zeroed so padded rows stay finite)
+  // The split count is not monotone in the prefix length, so the partials are
+  // sized for every (B, H, P) a later call may use; P enters only through the
+  // number of 32-key blocks.
   size_t part = 0;
   for (int B = 1; B <= m.max_batch; ++B)
-    for (int H = 1; H <= m.max_chunk; ++H) {
-      int bps;
-      const int sp = attn_splits(c, B, H, m.max_prefix, &bps);
-      if (sp > 1) {
-        const size_t rows_pad = (size_t)((c->Hq / c->Hkv) * H + 63) / 64 * 64;
-        part = std::max(part, (size_t)sp * B * c->Hkv * rows_pad);
+    for (int H = 1; H <= m.max_chunk; ++H)
+      for (int nb = (H + 31) / 32; nb <= (m.max_prefix + H + 31) / 32; ++nb) {
+        int bps;
+        const int sp = attn_splits_nb(c, B, H, nb, &bps);
+        if (sp > 1) {
+          const size_t rows_pad = (size_t)((c->Hq / c->Hkv) * H + 63) / 64 * 64;
+          part = std::max(part, (size_t)sp * B * c->Hkv * rows_pad);
+        }
       }
-    }
   c->attn_part_elems = part;
   const size_t M = c->m_alloc;
   Carve a;
@@ -302,7 +336,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
          o_trx0 = a.take<float>(M * Da), o_trv = a.take<float>(M * Da), o_trt = a.take<float>(kMaxTrSteps * M),
          o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M),
          o_mod = a.take<float>(M * c->n_mod), o_mshift = a.take<uint16_t>(c->ada ? (size_t)2 * c->L * M * d : 0),
-         o_pf = a.take<unsigned>(64);
+         o_pf = a.take<unsigned>(64), o_status = a.take<unsigned>(1);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -328,6 +362,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->mod = (float *)(ab + o_mod);
   c->mod_shift_ops = (op_t *)(ab + o_mshift);
   c->pf_sink = (unsigned *)(ab + o_pf);
+  c->status = (unsigned *)(ab + o_status);
   e = attention_init();
   if (e == hipSuccess) e = gemm_init();
   if (e != hipSuccess) {
@@ -337,6 +372,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->rel_stream, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_rel, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_out, hipEventDisableTiming);
   if (e != hipSuccess) {
     uad_destroy(c);
     return cerr(UAD_E_HIP, std::string("hipStreamCreate(capture/release): ") + hipGetErrorString(e));
@@ -367,6 +404,8 @@ void uad_destroy(uad_ctx *c) {
     (void)hipStreamDestroy(c->rel_stream);
   }
   if (c->ev_rel) (void)hipEventDestroy(c->ev_rel);
+  if (c->ev_in) (void)hipEventDestroy(c->ev_in);
+  if (c->ev_out) (void)hipEventDestroy(c->ev_out);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
 }
@@ -392,6 +431,9 @@ uad_status uad_load_weights(uad_ctx *c, const uad_tensor *ts, int32_t n) {
   if (!c) return UAD_E_INVALID;
   if (!ts || n < 1) return fail(c, UAD_E_INVALID, "uad_load_weights: no tensors");
   (void)hipSetDevice(c->device);
+  // queued steps may still read the weights being replaced
+  hipError_t se = hipStreamSynchronize(c->stream);
+  if (se != hipSuccess) return hip_fail(c, se, "uad_load_weights: hipStreamSynchronize");
   const int d = c->d, F = c->F, Da = c->Da;
   // required names and shapes
   std::map<std::string, std::vector<int64_t>> need;
@@ -559,6 +601,9 @@ uad_status uad_set_prefix_kv(uad_ctx *c, const void *k, const void *v, int32_t d
   if (batch > c->cfg.max_batch) return fail(c, UAD_E_SHAPE, "uad_set_prefix_kv: batch > max_batch");
   if (prefix_len > c->cfg.max_prefix) return fail(c, UAD_E_SHAPE, "uad_set_prefix_kv: prefix_len > max_prefix");
   (void)hipSetDevice(c->device);
+  // queued steps (a release's tail, say) may still read the K/V being replaced
+  hipError_t se = hipStreamSynchronize(c->stream);
+  if (se != hipSuccess) return hip_fail(c, se, "uad_set_prefix_kv: hipStreamSynchronize");
   const int L = c->L, Hkv = c->Hkv, hd = c->hd, P = prefix_len, S = c->s_alloc;
   const size_t per_layer_in = (size_t)batch * P * Hkv * hd;
   std::string err;
@@ -646,14 +691,16 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     };
     const int n_mod = c->n_mod;
     if (!c->ada) {
-      UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, s,
+      UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, c->status, s,
                                         ea_, eb_));
       GemmArgs g{};
+      g.status = c->status;
       g.M = M; g.m_alloc = (int)MA;
       g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = 2 * d;
       g.out = c->a_z; g.ldo = d; g.bias = c->t1_b;
       UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, 2 * d), s, ea_, eb_));
       GemmArgs g2{};
+      g2.status = c->status;
       g2.M = M; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d;
       g2.out = c->h; g2.ldo = d; g2.bias = c->t2_b; norm_fields(g2);
       g2.gain_next = c->layers[0].attn_norm; g2.next = c->a_n;
@@ -662,22 +709,26 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       // conditioning computed for the whole schedule: h_0 = W_in x + b_in and the
       // first attention norm's operand h_0 (1 + a) from this step's modulations
       UAD_CHECK_CLS(K_TEMB, launch_temb_ada(x, nullptr, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs,
-                                            c->a_te, c->h, c->ssq, (int)MA, s, ea_, eb_, pre->mod, n_mod, c->a_n));
+                                            c->a_te, c->h, c->ssq, (int)MA, c->status, s, ea_, eb_, pre->mod, n_mod,
+                                            c->a_n));
     } else {
       // adaptive norms: h_0 = W_in x + b_in, c = SiLU(W2 SiLU(W1 e(t) + b1) + b2), then every
       // modulation (a, b, g per norm site) in one GEMM whose epilogue also forms the
       // first attention norm's operand h_0 * (1 + a)
       UAD_CHECK_CLS(K_TEMB, launch_temb_ada(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te,
-                                            c->h, c->ssq, (int)MA, s, ea_, eb_));
+                                            c->h, c->ssq, (int)MA, c->status, s, ea_, eb_));
       GemmArgs g{};
+      g.status = c->status;
       g.M = M; g.m_alloc = (int)MA; g.A = c->a_te; g.W = c->t1_w; g.N = d; g.K = d; g.out = c->a_z; g.ldo = d;
       g.bias = c->t1_b;
       UAD_CHECK_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, M, d, d), s, ea_, eb_));
       GemmArgs g2{};
+      g2.status = c->status;
       g2.M = M; g2.m_alloc = (int)MA; g2.A = c->a_z; g2.W = c->t2_w; g2.N = d; g2.K = d; g2.out = c->a_te;
       g2.ldo = d; g2.bias = c->t2_b;
       UAD_CHECK_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_SILU, g2, plan_gemm(EPI_BIAS_SILU, M, d, d), s, ea_, eb_));
       GemmArgs gm{};
+      gm.status = c->status;
       gm.M = M; gm.m_alloc = (int)MA; gm.A = c->a_te; gm.W = c->w_mod; gm.N = n_mod; gm.K = d; gm.out = c->mod; gm.ldo = n_mod;
       gm.bias = c->b_mod; gm.mod_shift_ops = c->mod_shift_ops; gm.shift_stride = MA * d; gm.h_in = c->h;
       gm.d_model = d; gm.n_layers = c->L; gm.next = c->a_n;
@@ -685,10 +736,13 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     }
 
     AttnArgs at{};
+    at.status = c->status;
     at.q = c->q; at.ldq = c->q_dim; at.s_alloc = c->s_alloc; at.n_keys = c->prefix_len + H;
     at.chunk = H; at.n_heads = c->Hq; at.n_kv_heads = c->Hkv; at.group = c->Hq / c->Hkv;
     at.rows = at.group * H; at.rows_pad = (at.rows + 63) / 64 * 64;
     at.splits = attn_splits(c, B, H, c->prefix_len, &at.blocks_per_split);
+    if (attn_part_rows(c, B, H, c->prefix_len) > c->attn_part_elems)
+      return fail(c, UAD_E_SHAPE, "split-KV partials exceed the workspace sized at uad_create");
     at.qblocks = (at.rows + 63) / 64; at.n_eh = B * c->Hkv;
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
     at.o = c->a_o; at.ldo = c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
@@ -710,6 +764,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       __bf16 *kc = c->kcache + l * c->kv_layer_elems;
       __bf16 *vtc = c->vtcache + l * c->kv_layer_elems;
       GemmArgs q{};
+      q.status = c->status;
       q.M = M; q.A = c->a_n; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
@@ -738,6 +793,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       }
       UAD_CHECK_CLS(K_ATTENTION, launch_attention(at, B, c->hd, s, ea_, eb_));
       GemmArgs o{};
+      o.status = c->status;
       o.M = M; o.A = c->a_o; o.W = lp.wo; o.N = d; o.K = c->q_dim;
       o.out = c->h; o.ldo = d; norm_fields(o);
       o.gain_next = lp.mlp_norm; o.next = c->a_n;
@@ -747,11 +803,13 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       }
       UAD_CHECK_CLS(K_GEMM_O, launch_gemm(EPI_RESID_F32, o, po, s, ea_, eb_));
       GemmArgs gu{};
+      gu.status = c->status;
       gu.M = M; gu.A = c->a_n; gu.W = lp.wgu; gu.N = 2 * F; gu.K = d;
       gu.out = c->a_g; gu.ldo = F; norm_fields(gu); gu.use_rstd = 1;
       if (c->ada) gu.A2 = shift_base + (size_t)(2 * l + 1) * shift_stride;
       UAD_CHECK_CLS(K_GEMM_GATEUP, launch_gemm(EPI_GEGLU, gu, pg, s, ea_, eb_));
       GemmArgs dn{};
+      dn.status = c->status;
       dn.M = M; dn.A = c->a_g; dn.W = lp.wdown; dn.N = d; dn.K = F;
       dn.out = c->h; dn.ldo = d; norm_fields(dn);
       dn.gain_next = (l + 1 < c->L) ? c->layers[l + 1].attn_norm : nullptr; dn.next = c->a_n;
@@ -839,17 +897,20 @@ static uad_status enqueue_ada_schedule(uad_ctx *c, hipStream_t s, const GraphKey
     if (e != hipSuccess) return hip_fail(c, e, #call); \
     if (c->prof_on) c->prof_pending.push_back({cls, ea_, eb_}); \
   } while (0)
-  e = launch_time_features(k.t, M, (int)c->m_alloc, k.n_steps, d, c->freqs, c->pre_te, s);
+  e = launch_time_features(k.t, M, (int)c->m_alloc, k.n_steps, d, c->freqs, c->pre_te, c->status, s);
   if (e != hipSuccess) return hip_fail(c, e, "launch_time_features");
   GemmArgs g{};
+  g.status = c->status;
   g.M = rows; g.m_alloc = rows; g.A = c->pre_te; g.W = c->t1_w; g.N = d; g.K = d; g.out = c->pre_z; g.ldo = d;
   g.bias = c->t1_b;
   UAD_PRE_CLS(K_GEMM_TIME_IN, launch_gemm(EPI_BIAS_SILU, g, plan_gemm(EPI_BIAS_SILU, rows, d, d), s, ea_, eb_));
   GemmArgs g2{};
+  g2.status = c->status;
   g2.M = rows; g2.m_alloc = rows; g2.A = c->pre_z; g2.W = c->t2_w; g2.N = d; g2.K = d; g2.out = c->pre_te;
   g2.ldo = d; g2.bias = c->t2_b;
   UAD_PRE_CLS(K_GEMM_TIME_OUT, launch_gemm(EPI_BIAS_SILU, g2, plan_gemm(EPI_BIAS_SILU, rows, d, d), s, ea_, eb_));
   GemmArgs gm{};
+  gm.status = c->status;
   gm.M = rows; gm.m_alloc = rows; gm.A = c->pre_te; gm.W = c->w_mod; gm.N = c->n_mod; gm.K = d; gm.out = c->pre_mod;
   gm.ldo = c->n_mod; gm.bias = c->b_mod; gm.mod_shift_ops = c->pre_shift; gm.shift_stride = (size_t)rows * d;
   gm.h_in = nullptr; gm.next = nullptr; gm.d_model = d; gm.n_layers = c->L;
@@ -990,6 +1051,17 @@ static uad_status run_work(uad_ctx *c, GraphKey k) {
   return UAD_OK;
 }
 
+// run_work between the null-stream ordering points of a library-owned stream.
+static uad_status run_ordered(uad_ctx *c, const GraphKey &k) {
+  hipError_t e = order_before(c);
+  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
+  uad_status rs = run_work(c, k);
+  if (rs != UAD_OK) return rs;
+  e = order_after(c);
+  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
+  return UAD_OK;
+}
+
 uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
                             float *v_out, int32_t batch, int32_t chunk) {
   if (!c) return UAD_E_INVALID;
@@ -1000,7 +1072,7 @@ uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *d
   k.kind = 0;
   k.is_schedule = false;
   k.x = x; k.t = t; k.dt = dt; k.mask = mask; k.v_out = v_out; k.n_steps = 1; k.B = batch; k.H = chunk;
-  return run_work(c, k);
+  return run_ordered(c, k);
 }
 
 uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, const float *dt_sched,
@@ -1017,7 +1089,7 @@ uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, cons
   k.is_schedule = true;
   k.x = x; k.t = t_sched; k.dt = dt_sched; k.mask = mask_sched; k.n_steps = n_steps; k.B = batch; k.H = chunk;
   k.released = released; k.release_step = release_step; k.step_ticks = step_ticks;
-  return run_work(c, k);
+  return run_ordered(c, k);
 }
 
 uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chunk, int32_t U, int32_t K,
@@ -1088,6 +1160,8 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
   k.x = x; k.B = batch; k.H = chunk; k.n_steps = Nstar; k.step_ticks = step_ticks;
   k.U = U; k.Kr = K; k.Nstar = Nstar; k.S = S; k.reconcile = reconcile;
   k.urgent = urgent_out; k.executed = executed_out; k.gac_mask = gac_mask; k.urgent_host = host_dev;
+  hipError_t oe = order_before(c);
+  if (oe != hipSuccess) return hip_fail(c, oe, "stream ordering");
   uad_status rs = run_work(c, k);
   if (rs != UAD_OK) return rs;
   // release: the urgent actions (and their pinned host copy) are final here;
@@ -1106,7 +1180,11 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
   if (e != hipSuccess) return hip_fail(c, e, "uad_denoise_release: release");
   k.kind = 2;
   k.urgent_host = nullptr;
-  return run_work(c, k);
+  rs = run_work(c, k);
+  if (rs != UAD_OK) return rs;
+  e = order_after(c);
+  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
+  return UAD_OK;
 }
 
 uad_status uad_synchronize(uad_ctx *c) {
@@ -1114,7 +1192,18 @@ uad_status uad_synchronize(uad_ctx *c) {
   (void)hipSetDevice(c->device);
   hipError_t e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
-  return UAD_OK;
+  // the device status word of the work just finished (read, then cleared)
+  unsigned w = 0;
+  e = hipMemcpy(&w, c->status, sizeof(w), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(c, e, "uad_synchronize: status word");
+  if (w == 0) return UAD_OK;
+  e = hipMemset(c->status, 0, sizeof(w));
+  if (e != hipSuccess) return hip_fail(c, e, "uad_synchronize: status word");
+  if (w & kStatusTimeout)
+    return fail(c, UAD_E_HIP, "uad_synchronize: an in-kernel wait gave up (results of that work are invalid)");
+  return fail(c, UAD_E_RANGE,
+              "uad_synchronize: an fp16 GEMM / attention operand was not finite (|value| > 65504 or NaN); "
+              "results of that work are invalid");
 }
 
 uad_status uad_tick_rate_hz(uad_ctx *c, double *hz) {

@@ -54,7 +54,29 @@ constexpr int kTileN = 16;
 constexpr int kTileK = 32;
 constexpr int kBlockElems = kTileN * kTileK;  // 512 fp16 = 1 KiB
 
-__device__ __forceinline__ void store_op(op_t *p, float v) { *p = (op_t)v; }
+// Device status word of a context (bits, cleared and reported by
+// uad_synchronize): an fp16 operand that was not finite after rounding, and an
+// in-kernel wait that gave up.
+constexpr unsigned kStatusRange = 1u;
+constexpr unsigned kStatusTimeout = 2u;
+
+__device__ __forceinline__ void raise_status(unsigned *status, unsigned bit) {
+  __hip_atomic_fetch_or(status, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Every fp16 operand store checks its value: fp16 holds magnitudes below
+// 65520 (which round to at most 65504); anything larger becomes inf and a NaN
+// stays NaN, so both raise the context's range bit instead of passing silently.
+__device__ __forceinline__ void store_op(op_t *p, float v, unsigned *status) {
+  *p = (op_t)v;
+  if (!(__builtin_fabsf(v) < 65520.0f)) raise_status(status, kStatusRange);
+}
+__device__ __forceinline__ void check_op4(float a, float b, float c, float d, unsigned *status) {
+  const float T = 65520.0f;
+  const bool bad = !(__builtin_fabsf(a) < T) | !(__builtin_fabsf(b) < T) | !(__builtin_fabsf(c) < T) |
+                   !(__builtin_fabsf(d) < T);
+  if (bad) raise_status(status, kStatusRange);
+}
 
 // ---------------------------------------------------------------------------
 // Cross-lane reductions without the LDS crossbar (ds_bpermute): DPP within a
@@ -165,6 +187,7 @@ struct GemmArgs {
   __bf16 *kc;   // layer K store [B][Hkv][S_alloc][hd]
   __bf16 *vtc;  // layer V^T store, 32-key blocks (vt_index)
   int chunk, prefix, s_alloc, n_kv_heads, head_dim, q_dim;
+  unsigned *status;  // context status word (range bit of the fp16 operand stores)
 };
 
 // Up to two byte ranges (weights of the next projections) that otherwise idle
@@ -194,6 +217,7 @@ struct AttnArgs {
   Prefetch pre_attn;  // read by extra workgroups of the attention kernel
   Prefetch pre_comb;  // read by an extra slice of the split-merge grid (wgs: nonzero = on)
   unsigned *pf_sink;  // one word the prefetch may write (keeps its loads alive)
+  unsigned *status;   // context status word (range bit of the fp16 stores)
 };
 
 struct FinalArgs {
@@ -252,17 +276,17 @@ hipError_t gemm_init();                  // once per context: raise the batched 
 int attention_chunk_blocks(int head_dim);  // 32-key blocks loaded per round trip
 int attention_max_splits(int head_dim);    // split-KV partials the combine accepts
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
-                       const float *b_in, const float *freqs, op_t *te, hipStream_t s,
+                       const float *b_in, const float *freqs, op_t *te, unsigned *status, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // adaptive-norm variant: te <- e(t) (K = d); h <- W_in x + b_in with its
 // per-16-column sums of squares ssq[d/16][m_alloc]
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                            const float *b_in, const float *freqs, op_t *te, float *h, float *ssq, int m_alloc,
-                           hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
+                           unsigned *status, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
                            const float *mod_a0 = nullptr, int mod_ld = 0, op_t *next = nullptr);
 // sinusoidal time features of n_steps x m_alloc rows (rows past M in a step: time 0)
 hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps, int d, const float *freqs,
-                                op_t *te, hipStream_t s);
+                                op_t *te, unsigned *status, hipStream_t s);
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 hipError_t launch_stamp(uint64_t *dst, hipStream_t s);
 hipError_t launch_tr_init(const TrArgs &a, hipStream_t s);     // x0 <- x, vsum <- 0
@@ -371,6 +395,8 @@ struct uad_ctx {
   int tr_key[6] = {0, 0, 0, 0, 0, -1};         // B, H, U, K, N*, reconcile of the tables
   hipStream_t rel_stream = nullptr;            // release copies to pageable host memory
   hipEvent_t ev_rel = nullptr;
+  hipEvent_t ev_in = nullptr, ev_out = nullptr;  // null-stream ordering of a library-owned stream
+  unsigned *status = nullptr;                  // device status word (kStatusRange, kStatusTimeout)
 
   // captured step / schedule graphs (small LRU cache)
   struct GraphEntry {

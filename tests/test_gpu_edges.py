@@ -17,7 +17,7 @@ import torch
 
 import oracle as O
 import paper_2609_37772_amd as U
-from tests.harness import log, make_case, rel_err
+from tests.harness import log, make_case, prefix_stack_bf16, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -143,3 +143,60 @@ def test_tall_query_blocks_sampled_envs(gpu):
         log(f"[tiny B=40 H=128] env {b}: step-0 velocity rel err {e:.2e}, released abs err {ea:.2e}")
         assert e <= VEL_RTOL and ea <= ACT_ATOL
     np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
+
+
+def test_fp16_operand_overflow_raises_range_status(gpu):
+    """An activation beyond the fp16 range (the fp32 action input projection
+    scaled by 1e7, so that |W_in x| is far above 65504 in the time MLP's fp16
+    operand) raises UAD_E_RANGE at the next synchronisation instead of passing
+    as inf; the report clears the status, and in-range weights run clean."""
+    c = make_case("tiny", with_expert=False)
+    ex = U.ActionExpert(c.wl.shape, 1, c.wl.chunk, c.wl.prefix)
+    try:
+        K, V = prefix_stack_bf16(c)
+        ex.set_prefix_kv(K, V, 1, c.wl.prefix)
+        big = dict(c.weights)
+        big["action_in.w"] = (c.weights["action_in.w"] * np.float32(1e7)).astype(np.float32)
+        ex.load_weights(big)
+        n, t, dt, mask = O.build_schedule(c.budgets)
+        x = dev(c.noise.astype(np.float32))
+        ex.step(x, dev(t[0]), dev(dt[0]), dev(mask[0]))
+        with pytest.raises(U.UadError) as ei:
+            ex.synchronize()
+        assert ei.value.status == 8 and "65504" in str(ei.value)
+        ex.synchronize()  # reported once, then cleared
+        ex.load_weights(c.weights)
+        x = dev(c.noise.astype(np.float32))
+        v = torch.empty_like(x)
+        ex.step(x, dev(t[0]), dev(dt[0]), dev(mask[0]), v)
+        ex.synchronize()
+        assert torch.isfinite(v).all()
+    finally:
+        ex.close()
+
+
+def test_split_partials_sized_for_every_prefix(gpu):
+    """A context for prefixes up to 2048 keys, called with 2 environments, a
+    71-action chunk and a 1722-key prefix: that call splits the keys 15 ways,
+    more than the longest prefix does (14), since the split count is not
+    monotone in the prefix length.  The workspace is sized over every prefix
+    length, and the step matches the oracle."""
+    c = make_case("tiny", with_expert=False, batch=2, chunk=71, prefix=1722)
+    ex = U.ActionExpert(c.wl.shape, 2, 128, 2048)
+    try:
+        ex.load_weights(c.weights)
+        K, V = prefix_stack_bf16(c)
+        ex.set_prefix_kv(K, V, 2, 1722)
+        n, t, dt, mask = O.build_schedule(c.budgets)
+        v_ref = O.velocity(c.oracle_model(), c.noise, t[0])
+        x = dev(c.noise.astype(np.float32))
+        v = torch.empty_like(x)
+        ex.step(x, dev(t[0]), dev(dt[0]), dev(mask[0]), v)
+        ex.synchronize()
+        v = v.cpu().numpy()
+        for b in range(2):
+            e = rel_err(v[b], v_ref[b])
+            log(f"[P=1722 of 2048, H=71, B=2] env {b}: velocity rel err {e:.2e}")
+            assert e <= VEL_RTOL
+    finally:
+        ex.close()
