@@ -179,6 +179,20 @@ uad_status uad_set_prefix_kv(uad_ctx *ctx, const void *k, const void *v, int32_t
 uad_status uad_denoise_step(uad_ctx *ctx, float *x, const float *t, const float *dt,
                             const uint8_t *mask, float *v_out, int32_t batch, int32_t chunk);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * joint step as uad_denoise_step, with the same arguments, results (bit for
+ * bit) and errors, that allocates nothing.  Its kernels are launched directly
+ * on the context's stream (no graph is captured or instantiated) and the
+ * attention's split-KV partials use a static device array of 8 MiB per GPU,
+ * held until the process ends, instead of the context's workspace.  A call
+ * whose batch, chunk and prefix need more than that is refused with
+ * UAD_E_SHAPE before any work.  Every context on a GPU shares that GPU's
+ * array: calls that overlap on one GPU (other streams, other contexts) race;
+ * the array needs no clearing between calls. */
+uad_status uad_denoise_step_static(uad_ctx *ctx, float *x, const float *t, const float *dt,
+                                   const uint8_t *mask, float *v_out, int32_t batch, int32_t chunk);
+
 /* A whole per-token schedule (Sec. 4.2 Eqs. 4-5): n_steps joint steps, step k
  * using the k-th slice of the tables.
  *   x                     device fp32 [batch][chunk][Da], in/out (x_0 in, final out)

@@ -17,9 +17,9 @@ import torch  # loaded first on purpose: libuad then binds to PyTorch's HIP runt
 __all__ = [
     "LIB_PATH", "EXPORTED_SYMBOLS", "UadError", "load_library", "library_loaded",
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
-    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_denoise_release",
-    "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
-    "uad_profile_enable", "uad_profile_read", "UAD_DTYPE_F32", "UAD_DTYPE_BF16", "STATUS_NAMES",
+    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_step_static", "uad_denoise_schedule",
+    "uad_denoise_release", "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz",
+    "uad_debug_velocity_field", "uad_profile_enable", "uad_profile_read", "UAD_DTYPE_F32", "UAD_DTYPE_BF16", "STATUS_NAMES",
     "UAD_RELEASE_UAER", "UAD_RELEASE_TR", "UAD_FLAG_ADARMS",
 ]
 
@@ -31,7 +31,7 @@ STATUS_NAMES = {0: "UAD_OK", 1: "UAD_E_INVALID", 2: "UAD_E_SHAPE", 3: "UAD_E_STA
                 5: "UAD_E_HIP", 6: "UAD_E_OOM", 7: "UAD_E_UNSUPPORTED", 8: "UAD_E_RANGE"}
 EXPORTED_SYMBOLS = [
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
-    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_schedule", "uad_denoise_release",
+    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_step_static", "uad_denoise_schedule", "uad_denoise_release",
     "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
     "uad_profile_enable", "uad_profile_read",
 ]
@@ -75,6 +75,7 @@ def load_library() -> ctypes.CDLL:
         "uad_load_weights": ([P, ctypes.POINTER(uad_tensor), I32], I32),
         "uad_set_prefix_kv": ([P, P, P, I32, I32, I32, I32], I32),
         "uad_denoise_step": ([P, P, P, P, P, P, I32, I32], I32),
+        "uad_denoise_step_static": ([P, P, P, P, P, P, I32, I32], I32),
         "uad_denoise_schedule": ([P, P, P, P, P, I32, I32, I32, P, P, P], I32),
         "uad_denoise_release": ([P, P, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P, P], I32),
         "uad_build_schedule": ([P, I32, I32, I32, P, P, P, P], I32),
@@ -227,6 +228,16 @@ def uad_denoise_step(ctx: int, x: torch.Tensor, t: torch.Tensor, dt: torch.Tenso
          _dev_ptr(dt, torch.float32, (B, H), "dt"), _dev_ptr(mask, torch.uint8, (B, H), "mask"),
          _dev_ptr(v_out, torch.float32, (B, H, Da), "v_out")]
     _check(ctx, load_library().uad_denoise_step(ctx, *p, B, H), "uad_denoise_step")
+
+
+def uad_denoise_step_static(ctx: int, x: torch.Tensor, t: torch.Tensor, dt: torch.Tensor, mask: torch.Tensor,
+                            v_out: Optional[torch.Tensor] = None) -> None:
+    """uad_denoise_step without any allocation (split-KV scratch in a static device array)."""
+    B, H, Da = x.shape
+    p = [_dev_ptr(x, torch.float32, (B, H, Da), "x"), _dev_ptr(t, torch.float32, (B, H), "t"),
+         _dev_ptr(dt, torch.float32, (B, H), "dt"), _dev_ptr(mask, torch.uint8, (B, H), "mask"),
+         _dev_ptr(v_out, torch.float32, (B, H, Da), "v_out")]
+    _check(ctx, load_library().uad_denoise_step_static(ctx, *p, B, H), "uad_denoise_step_static")
 
 
 def uad_denoise_schedule(ctx: int, x: torch.Tensor, t_sched: torch.Tensor, dt_sched: torch.Tensor,

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -172,6 +173,44 @@ hipError_t order_after(uad_ctx *c) {
   hipError_t e = hipEventRecord(c->ev_out, c->stream);
   if (e == hipSuccess) e = hipStreamWaitEvent(nullptr, c->ev_out, 0);
   return e;
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the no-allocation step (uad_denoise_step_static): the split-KV
+// partials live in this file-scope device array, one copy per GPU, held until
+// the process ends.  Host code never passes the array's name to a kernel (on
+// the host it is a stand-in, not a device address): uad_create looks up each
+// device's address once, with that device current, and the entry point passes
+// that address.  Calls that overlap on one GPU share the array and race.
+// ---------------------------------------------------------------------------
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];        // device address of `scratch` per device (null: not looked up)
+hipError_t g_scratch_err[kMaxDevices];   // result of the failed lookup, reported by the entry point
+
+// Once per device, with that device current: the device address of `scratch`.
+hipError_t static_scratch_lookup(int device) {
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[device]) return hipSuccess;
+  void *p = nullptr;
+  hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  g_scratch_err[device] = e;
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  g_scratch_ptr[device] = p;
+  return hipSuccess;
+}
+
+void *static_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  return g_scratch_ptr[device];
 }
 
 }  // namespace
@@ -365,6 +404,9 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->status = (unsigned *)(ab + o_status);
   e = attention_init();
   if (e == hipSuccess) e = gemm_init();
+  // the no-allocation step's scratch: its address on this device (a failure is
+  // reported by that entry point, the rest of the library does not need it)
+  if (e == hipSuccess) (void)static_scratch_lookup(device);
   if (e != hipSuccess) {
     uad_destroy(c);
     return cerr(UAD_E_HIP, std::string("attention kernel set-up: ") + hipGetErrorString(e));
@@ -664,25 +706,34 @@ struct AdaSlice {
   size_t shift_stride;     // elements from one [layer][norm] shift operand to the next
 };
 
+// Split-KV partials of a step in caller-chosen memory instead of the context's
+// workspace (the no-allocation entry point), and no measurement events.
+struct StepScratch {
+  op_t *opart;
+  float *mlpart;
+};
+
 static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float *t, const float *dt,
                                const uint8_t *mask, const uint8_t *next_mask, int is_last, int step, float *v_out,
                                float *released, int32_t *release_step, int B, int H, float *vsum = nullptr,
-                               int vsum_tokens = 0, const AdaSlice *pre = nullptr) {
+                               int vsum_tokens = 0, const AdaSlice *pre = nullptr,
+                               const StepScratch *scratch = nullptr) {
   const int M = B * H, d = c->d, F = c->F;
   const size_t MA = c->m_alloc;
+  const bool prof = c->prof_on && !scratch;
   hipError_t e = hipSuccess;
   // measurement hook: the launch records a start/stop event pair taken from
   // the kernel's own dispatch packet (ea_/eb_ are nullptr when not profiling)
 #define UAD_CHECK_CLS(cls, call)                       \
   do {                                                 \
     hipEvent_t ea_ = nullptr, eb_ = nullptr;           \
-    if (c->prof_on) {                                  \
+    if (prof) {                                        \
       ea_ = pool_event(c);                             \
       eb_ = pool_event(c);                             \
     }                                                  \
     e = (call);                                        \
     if (e != hipSuccess) return hip_fail(c, e, #call); \
-    if (c->prof_on) c->prof_pending.push_back({cls, ea_, eb_}); \
+    if (prof) c->prof_pending.push_back({cls, ea_, eb_}); \
   } while (0)
   if (!c->dbg) {
     // RMSNorm folding: residual GEMMs write ssq and the next operand; consumers scale by rstd
@@ -741,11 +792,13 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     at.chunk = H; at.n_heads = c->Hq; at.n_kv_heads = c->Hkv; at.group = c->Hq / c->Hkv;
     at.rows = at.group * H; at.rows_pad = (at.rows + 63) / 64 * 64;
     at.splits = attn_splits(c, B, H, c->prefix_len, &at.blocks_per_split);
-    if (attn_part_rows(c, B, H, c->prefix_len) > c->attn_part_elems)
+    if (!scratch && attn_part_rows(c, B, H, c->prefix_len) > c->attn_part_elems)
       return fail(c, UAD_E_SHAPE, "split-KV partials exceed the workspace sized at uad_create");
     at.qblocks = (at.rows + 63) / 64; at.n_eh = B * c->Hkv;
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
-    at.o = c->a_o; at.ldo = c->q_dim; at.opart = c->attn_opart; at.mlpart = c->attn_ml;
+    at.o = c->a_o; at.ldo = c->q_dim;
+    at.opart = scratch ? scratch->opart : c->attn_opart;
+    at.mlpart = scratch ? scratch->mlpart : c->attn_ml;
     at.pf_sink = c->pf_sink;
     // Weight prefetch on otherwise idle CUs: when the attention leaves CUs free
     // (batch 1), its extra workgroups read the layer's O and gate/up weights and
@@ -1073,6 +1126,37 @@ uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *d
   k.is_schedule = false;
   k.x = x; k.t = t; k.dt = dt; k.mask = mask; k.v_out = v_out; k.n_steps = 1; k.B = batch; k.H = chunk;
   return run_ordered(c, k);
+}
+
+uad_status uad_denoise_step_static(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
+                                   float *v_out, int32_t batch, int32_t chunk) {
+  if (!c) return UAD_E_INVALID;
+  const char *fn = "uad_denoise_step_static";
+  uad_status st = check_step_args(c, x, t, dt, mask, batch, chunk, fn);
+  if (st != UAD_OK) return st;
+  (void)hipSetDevice(c->device);
+  char *base = (char *)static_scratch(c->device);
+  if (!base)
+    return fail(c, UAD_E_HIP, std::string(fn) + ": hipGetSymbolAddress(scratch) failed on this device: " +
+                                  (c->device < kMaxDevices ? hipGetErrorString(g_scratch_err[c->device])
+                                                           : "device index beyond the lookup table"));
+  const size_t rows = attn_part_rows(c, batch, chunk, c->prefix_len);
+  const size_t o_bytes = align256(rows * c->hd * sizeof(op_t));
+  const size_t need = o_bytes + rows * 2 * sizeof(float);
+  if (need > kStaticScratchBytes)
+    return fail(c, UAD_E_SHAPE, std::string(fn) + ": this batch, chunk and prefix need " + std::to_string(need) +
+                                    " bytes of split-KV scratch; the static array holds " +
+                                    std::to_string(kStaticScratchBytes));
+  const StepScratch sc{(op_t *)base, (float *)(base + o_bytes)};
+  hipError_t e = order_before(c);
+  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
+  // direct launches on the context stream: no graph capture or instantiation
+  st = enqueue_step(c, c->stream, x, t, dt, mask, nullptr, 0, 0, v_out, nullptr, nullptr, batch, chunk, nullptr, 0,
+                    nullptr, &sc);
+  if (st != UAD_OK) return st;
+  e = order_after(c);
+  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
+  return UAD_OK;
 }
 
 uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, const float *dt_sched,
