@@ -247,6 +247,167 @@ def _cpu_baseline_run(wl, weights, prefix, noise, budgets, seconds, threads, O):
             "seconds": el}
 
 
+def measure(ex, wl, budgets, noise, steps_req, warmup_req, sched_reps, U, np, torch):
+    """Time exactly ``steps_req`` joint steps after exactly ``warmup_req`` untimed
+    ones: whole schedules replayed from their captured graph, the remainder as
+    single steps of the next schedule slices; then per-schedule device time and
+    per-kernel-class launch times of the dominant class against its roofline."""
+    s = wl.shape
+    M = wl.batch * wl.chunk
+    n, tg, dtg, mg = ex.schedule_tables(budgets)
+    x0 = torch.from_numpy(noise).cuda()
+    x = torch.empty_like(x0)
+
+    def run(k_steps):
+        full, rem = divmod(k_steps, n)
+        for _ in range(full):
+            x.copy_(x0)
+            ex.schedule(x, tg, dtg, mg)
+        if rem:
+            x.copy_(x0)
+            for k in range(rem):
+                ex.step(x, tg[k], dtg[k], mg[k])
+
+    # Warm-up: exactly the requested steps when they also build every graph the
+    # timed region replays (a whole schedule when it times schedules, a single
+    # step when it times a remainder); otherwise the few extra steps that do,
+    # and the count actually run is reported.
+    steps = max(1, steps_req)
+    warm = max(0, warmup_req)
+    if steps >= n and warm < n:
+        warm = n + (warm % n if steps % n else 0)
+    if steps % n and warm % n == 0:
+        warm += 1
+    run(warm)
+    torch.cuda.synchronize()
+    log(f"[bench] {wl.name}: warm-up {warm} steps done (requested {warmup_req})")
+    t0 = time.perf_counter()
+    run(steps)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    sps = steps / el
+    ms_step = 1e3 * el / steps
+    log(f"[bench] {wl.name}: timed {steps} steps: {ms_step:.4f} ms/step, {sps:.1f} steps/s")
+
+    # Per-schedule device time (ticks at schedule start / end), median and a 95%
+    # bootstrap interval over the R schedules (8000 resamples).
+    hz = ex.tick_rate_hz()
+    ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
+    per_sched = []
+    for _ in range(max(1, sched_reps)):
+        x.copy_(x0)
+        ex.schedule(x, tg, dtg, mg, None, None, ticks)
+        torch.cuda.synchronize()
+        tk = ticks.numpy().astype(np.int64)
+        per_sched.append((tk[-1] - tk[0]) / hz * 1e3)
+    per_sched = np.array(per_sched)
+    rng = np.random.default_rng(0)
+    boot = np.median(rng.choice(per_sched, size=(8000, per_sched.size), replace=True), axis=1)
+    sched_stats = {"schedules": int(per_sched.size), "steps_per_schedule": int(n),
+                   "median_ms": round(float(np.median(per_sched)), 4),
+                   "ci95_ms": [round(float(np.percentile(boot, 2.5)), 4), round(float(np.percentile(boot, 97.5)), 4)],
+                   "clock": "device wall-clock ticks around each schedule (stamp kernels)"}
+    log(f"[bench] {wl.name}: schedule median {sched_stats['median_ms']} ms, 95% CI {sched_stats['ci95_ms']}")
+
+    # Per-kernel durations: the same schedules again, launched directly with a
+    # start/stop HIP event pair taken from each kernel's dispatch packet, on the
+    # stream the kernels run on (the library's measurement hook).
+    U.uad_profile_enable(ex.ctx, True)
+    run(max(n, (steps // n) * n))
+    prof = U.uad_profile_read(ex.ctx)
+    U.uad_profile_enable(ex.ctx, False)
+    kb, kf = kernel_bytes(wl, M), kernel_flops(wl, M)
+    per_kernel = {}
+    for name, (ms, cnt) in prof.items():
+        if cnt == 0:
+            continue
+        avg_us = 1e3 * ms / cnt
+        ent = {"avg_us": round(avg_us, 3), "launches": cnt, "share": None}
+        if name in kb:
+            ent["gbs"] = round(kb[name] / (avg_us * 1e-6) / 1e9, 1)
+            ent["tflops"] = round(kf[name] / (avg_us * 1e-6) / 1e12, 2)
+        per_kernel[name] = ent
+    tot = sum(v[0] for v in prof.values()) or 1.0
+    for name in per_kernel:
+        per_kernel[name]["share"] = round(prof[name][0] / tot, 4)
+    dom = max((k for k in per_kernel if k in kb), key=lambda k: prof[k][0])
+    dom_us = per_kernel[dom]["avg_us"]
+    batched = M > 400
+    if batched:
+        ach = kf[dom] / (dom_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4),
+                "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None,
+                "algorithmic_flops_per_launch": kf[dom]}
+    else:
+        ach = kb[dom] / (dom_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None}
+    roof.update({"kernel": dom, "algorithmic_bytes_per_launch": kb[dom], "avg_launch_us": dom_us})
+    if dom == "attention" and not batched:
+        # at batch 1 the attention launches carry the read-ahead of the next
+        # projections' weights (O, gate/up, down, next layer's QKV) on the CUs they
+        # leave idle: part of their measured traffic, none of their algorithmic bytes
+        d, F, qd = s.d_model, s.d_ff, s.n_heads * s.head_dim
+        nqkv = qd + 2 * s.n_kv_heads * s.head_dim
+        roof["prefetch_bytes_per_launch"] = 2 * (d * qd + 2 * F * d + d * F + nqkv * d)
+    log(f"[bench] {wl.name}: dominant kernel {dom}: {dom_us:.2f} us/launch, {roof['achieved']} {roof['unit']}")
+    return {"steps_per_s": sps, "ms_per_step": ms_step, "steps": steps, "warmup": warm, "n": n,
+            "roofline": roof, "kernels": per_kernel, "schedule_time": sched_stats}
+
+
+def device_inputs(wl, U, W, np, torch):
+    """Seeded synthetic inputs of a batched workload drawn on the device (the
+    same distributions as the host generator the parity tests use: weights
+    N(0, 0.02) and norm gains 1 + N(0, 0.02), prefix K/V and noise N(0, 1),
+    bf16-rounded), so that a benchmark leg does not spend minutes in host RNG."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(wl.seed + 7919)
+    s = wl.shape
+    weights = {}
+    for name, shp, kind in W.weight_specs(s):
+        z = torch.randn(shp, generator=g, device="cuda", dtype=torch.float32) * 0.02
+        weights[name] = (z + 1.0 if kind == "gain" else z).to(torch.bfloat16)
+    B, P = wl.batch, wl.prefix
+    shape = (s.n_layers, B, P, s.n_kv_heads, s.head_dim)
+    k = torch.randn(shape, generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn(shape, generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    noise = torch.randn((B, wl.chunk, s.action_dim), generator=g, device="cuda", dtype=torch.float32)
+    return weights, k, v, noise.cpu().numpy()
+
+
+def batched_leg(name, a, U, W, np, torch):
+    """One batched (MFMA-bound) workload measured in the same run: ms per joint
+    step, environment-steps per second, whole-step MFMA fraction and the
+    dominant kernel class against the dense bf16 MFMA peak."""
+    wl = W.get_workload(name)
+    s = wl.shape
+    t0 = time.time()
+    weights, k, v, noise = device_inputs(wl, U, W, np, torch)
+    ex = U.ActionExpert(s, wl.batch, wl.chunk, wl.prefix)
+    ex.load_weights(weights)
+    ex.set_prefix_kv(k, v, wl.batch, wl.prefix)
+    del weights, k, v
+    torch.cuda.synchronize()
+    log(f"[bench] {name}: set-up {time.time() - t0:.1f} s (inputs drawn on the device)")
+    steps = max(a.steps, 20)
+    meas = measure(ex, wl, W.make_budgets(wl), noise, steps, a.warmup, min(a.sched_reps, 20), U, np, torch)
+    ex.close()
+    torch.cuda.empty_cache()
+    fl = step_flops(wl)
+    ms = meas["ms_per_step"]
+    return {"config": {"workload": name, "batch": wl.batch, "chunk": wl.chunk, "prefix": wl.prefix,
+                       "layers": s.n_layers, "width": s.d_model,
+                       "heads": f"{s.n_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.d_ff,
+                       "schedule": f"{wl.budget_kind} {meas['n']} steps"},
+            "ms_per_step": round(ms, 4), "env_steps_per_s": round(wl.batch * 1e3 / ms, 1),
+            "steps": meas["steps"], "warmup": meas["warmup"],
+            "flops_per_step": fl, "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
+            "roofline": meas["roofline"], "kernels": meas["kernels"], "schedule_time": meas["schedule_time"],
+            "data": "synthetic, drawn on the device (seeded torch generator, same distributions)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -258,6 +419,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-aal", action="store_true")
+    ap.add_argument("--no-batched", action="store_true",
+                    help="skip the batched (MFMA-bound) legs: 64-environment fleet and the large expert")
     ap.add_argument("--sched-reps", type=int, default=100,
                     help="schedules timed one by one for the median / bootstrap interval (fewer for profiler runs)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
@@ -305,90 +468,9 @@ def main():
     del K, V
     log(f"[bench] set-up {time.time() - t0:.1f} s")
 
-    n, tg, dtg, mg = ex.schedule_tables(budgets)
-    x0 = torch.from_numpy(noise).cuda()
-    x = torch.empty_like(x0)
-
-    def run(n_sched):
-        for _ in range(n_sched):
-            x.copy_(x0)
-            ex.schedule(x, tg, dtg, mg)
-
-    n_warm = max(1, -(-a.warmup // n))
-    n_timed = max(1, -(-a.steps // n))
-    steps = n_timed * n
-    run(n_warm)
-    torch.cuda.synchronize()
-    log(f"[bench] warm-up {n_warm * n} steps done")
-    t0 = time.perf_counter()
-    run(n_timed)
-    torch.cuda.synchronize()
-    el = time.perf_counter() - t0
-    sps = steps / el
-    ms_step = 1e3 * el / steps
-    log(f"[bench] timed {steps} steps: {ms_step:.4f} ms/step, {sps:.1f} steps/s")
-
-    # Per-schedule device time (ticks at schedule start / end), median and a 95%
-    # bootstrap interval over the R schedules (8000 resamples).
-    hz = ex.tick_rate_hz()
-    ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
-    per_sched = []
-    for _ in range(max(1, a.sched_reps)):
-        x.copy_(x0)
-        ex.schedule(x, tg, dtg, mg, None, None, ticks)
-        torch.cuda.synchronize()
-        tk = ticks.numpy().astype(np.int64)
-        per_sched.append((tk[-1] - tk[0]) / hz * 1e3)
-    per_sched = np.array(per_sched)
-    rng = np.random.default_rng(0)
-    boot = np.median(rng.choice(per_sched, size=(8000, per_sched.size), replace=True), axis=1)
-    sched_stats = {"schedules": int(per_sched.size), "steps_per_schedule": int(n),
-                   "median_ms": round(float(np.median(per_sched)), 4),
-                   "ci95_ms": [round(float(np.percentile(boot, 2.5)), 4), round(float(np.percentile(boot, 97.5)), 4)],
-                   "clock": "device wall-clock ticks around each schedule (stamp kernels)"}
-    log(f"[bench] schedule median {sched_stats['median_ms']} ms, 95% CI {sched_stats['ci95_ms']}")
-
-    # Per-kernel durations: the same schedules again, launched directly with a
-    # start/stop HIP event pair taken from each kernel's dispatch packet, on the
-    # stream the kernels run on (the library's measurement hook).
-    U.uad_profile_enable(ex.ctx, True)
-    run(n_timed)
-    prof = U.uad_profile_read(ex.ctx)
-    U.uad_profile_enable(ex.ctx, False)
-    kb, kf = kernel_bytes(wl, M), kernel_flops(wl, M)
-    per_kernel = {}
-    for name, (ms, cnt) in prof.items():
-        if cnt == 0:
-            continue
-        avg_us = 1e3 * ms / cnt
-        ent = {"avg_us": round(avg_us, 3), "launches": cnt, "share": None}
-        if name in kb:
-            ent["gbs"] = round(kb[name] / (avg_us * 1e-6) / 1e9, 1)
-            ent["tflops"] = round(kf[name] / (avg_us * 1e-6) / 1e12, 2)
-        per_kernel[name] = ent
-    tot = sum(v[0] for v in prof.values()) or 1.0
-    for name in per_kernel:
-        per_kernel[name]["share"] = round(prof[name][0] / tot, 4)
-    dom = max((k for k in per_kernel if k in kb), key=lambda k: prof[k][0])
-    dom_us = per_kernel[dom]["avg_us"]
-    batched = M > 400
-    if batched:
-        ach = kf[dom] / (dom_us * 1e-6) / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4), "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None}
-    else:
-        ach = kb[dom] / (dom_us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom) if wl.name == "pi0_b1" else None}
-    roof.update({"kernel": dom, "algorithmic_bytes_per_launch": kb[dom], "avg_launch_us": dom_us})
-    if dom == "attention" and not batched:
-        # at batch 1 the attention launches carry the read-ahead of the next
-        # projections' weights (O, gate/up, down, next layer's QKV) on the CUs they
-        # leave idle: part of their measured traffic, none of their algorithmic bytes
-        s = wl.shape
-        d, F, qd = s.d_model, s.d_ff, s.n_heads * s.head_dim
-        nqkv = qd + 2 * s.n_kv_heads * s.head_dim
-        roof["prefetch_bytes_per_launch"] = 2 * (d * qd + 2 * F * d + d * F + nqkv * d)
+    meas = measure(ex, wl, budgets, noise, a.steps, a.warmup, a.sched_reps, U, np, torch)
+    sps, ms_step, steps = meas["steps_per_s"], meas["ms_per_step"], meas["steps"]
+    roof, per_kernel, sched_stats, n = meas["roofline"], meas["kernels"], meas["schedule_time"], meas["n"]
     sb = step_bytes(wl)
     copy_gbs = streaming_copy_gbs(torch)
     step_roof = {"bytes_per_step": sb, "achieved_gbs": round(sb / (ms_step * 1e-3) / 1e9, 1),
@@ -397,21 +479,28 @@ def main():
                  "copy_frac": round(sb / (ms_step * 1e-3) / 1e9 / copy_gbs, 4),
                  "flops_per_step": step_flops(wl),
                  "mfma_frac": round(step_flops(wl) / (ms_step * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)}
-    log(f"[bench] dominant kernel {dom}: {dom_us:.2f} us/launch, {roof['achieved']} {roof['unit']}")
 
     out = {
         "metric": "denoise steps/sec + action-availability latency (ms) at B=1; % HBM/MFMA roofline",
-        "value": round(sps, 2), "unit": "denoise steps/s", "n_gpus": 1, "steps": steps, "warmup": n_warm * n,
+        "value": round(sps, 2), "unit": "denoise steps/s", "n_gpus": 1, "steps": steps, "warmup": meas["warmup"],
         "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded random-init weights, N(0,1) prefix K/V and noise)",
+        "dtype": "bf16 weights, fp16 MFMA operands (fp32 accumulation, fp32 residual and integrator)",
+        "data": "synthetic (seeded random-init weights, N(0,1) prefix K/V and noise)",
         "config": {"workload": wl.name, "batch": B, "chunk": H, "prefix": P, "layers": s.n_layers,
                    "width": s.d_model, "heads": f"{s.n_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.d_ff,
                    "action_dim": s.action_dim, "schedule": f"{wl.budget_kind} {n} steps"},
         "roofline": roof, "step_roofline": step_roof, "schedule_time": sched_stats, "kernels": per_kernel,
+        "kernels_clock": "direct-launch pass: the timed schedules again, each kernel launched on its own "
+                         "with start/stop events from its dispatch packet (no graph)",
     }
-
     if not a.no_aal and B == 1:
         out["availability"] = availability(ex, wl, noise, U, np, torch)
+    ex.close()
+
+    if not a.no_batched and wl.name == "pi0_b1":
+        out["batched"] = {}
+        for name in ("pi0_fleet_b64", "large_b16"):
+            out["batched"][name] = batched_leg(name, a, U, W, np, torch)
 
     if not a.no_cpu_baseline:
         log("[bench] timing the oracle on the host cores")
@@ -427,7 +516,6 @@ def main():
         torch.cuda.synchronize()
         out["copy_calibration"] = {"bytes_read": n * 4, "bytes_written": n * 4, "launches": 3}
     print(json.dumps(out), flush=True)
-    ex.close()
 
 
 def availability(ex, wl, noise, U, np, torch, reps=20):
