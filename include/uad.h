@@ -116,10 +116,10 @@ typedef struct {
   int32_t on_device; /* 1 if data is a device pointer */
 } uad_tensor;
 
-/* Create a context on HIP device `device`.  `hip_stream` is a hipStream_t on
- * that device, or NULL to let the library create its own; the work of a
- * library-owned stream is ordered after what the caller queued on the null
- * stream before each call, and the null stream's later work after it.  Allocates the
+/* Create a context on HIP device `device`.  `hip_stream` is the hipStream_t
+ * on that device the context enqueues its work on; NULL selects the device's
+ * null stream, so the work is ordered with everything else the caller (or
+ * PyTorch's default stream) queues there.  Allocates the
  * weight store, the prefix/chunk K/V store and all activation workspace for
  * the configured maxima.  Errors: UAD_E_INVALID (null/negative fields),
  * UAD_E_UNSUPPORTED (dimension the kernels cannot tile), UAD_E_OOM, UAD_E_HIP.
@@ -133,7 +133,8 @@ void uad_destroy(uad_ctx *ctx);
  * With ctx == NULL: the message of the last failed uad_create on this thread. */
 const char *uad_last_error(const uad_ctx *ctx);
 
-/* Re-target the context at another stream of the same device (NULL: own). */
+/* Re-target the context at another stream of the same device (NULL: the
+ * null stream), after its queued work is done. */
 uad_status uad_set_stream(uad_ctx *ctx, void *hip_stream);
 
 /* Load the action-expert parameters theta of F_theta (Sec. 3 Eq. 1).

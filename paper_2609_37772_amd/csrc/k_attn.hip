@@ -281,6 +281,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
   float lr[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) lr[r] = __shfl(l_tot, (lane >> 4) * 4 + r);
+  unsigned bad = 0;  // fp16 range flag of this lane's stores
   if (a.splits == 1) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -292,8 +293,9 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
       const float inv = 1.0f / lr[r];
 #pragma unroll
       for (int nt = 0; nt < NTO; ++nt)
-        store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv, a.status);
+        store_op(a.o + afrag_index(orow, head * HD + nt * 16 + (lane & 15), a.ldo / kTileK), o[nt][r] * inv, bad);
     }
+    flush_range(a.status, bad);
   } else {
     // Partials o_s / l_s in fp16 (bounded by max |V|), in the accumulator's
     // own layout: per 16-row tile, [nt][lane][4] (one 8-byte store per lane and
@@ -307,10 +309,11 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
     for (int nt = 0; nt < NTO; ++nt) {
       const float p0 = o[nt][0] * inv[0], p1 = o[nt][1] * inv[1], p2 = o[nt][2] * inv[2], p3 = o[nt][3] * inv[3];
       *(f16x4 *)(op + nt * 256) = f16x4{(op_t)p0, (op_t)p1, (op_t)p2, (op_t)p3};
-      check_op4(p0, p1, p2, p3, a.status);
+      check_op4(p0, p1, p2, p3, bad);
     }
     // lanes 0..15 hold the statistics of their own query row r0 + lane
     if (lane < 16) *(float2 *)(a.mlpart + (tile * 16 + lane) * 2) = float2{m_run, l_tot};
+    flush_range(a.status, bad);
   }
 }
 
@@ -334,6 +337,7 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
   const int ntiles = a.rows_pad / 16;
   const int lane = threadIdx.x;
   const int rbase = (lane >> 4) * 4;
+  unsigned bad = 0;  // fp16 range flag of this lane's stores
   f16x4 os[SMAX];
   float2 ml[SMAX][4];
 #pragma unroll
@@ -367,8 +371,9 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
     const int hg = row / a.chunk, tok = row - hg * a.chunk;
     const int head = g * a.group + hg;
     store_op(a.o + afrag_index(b * a.chunk + tok, head * hd + nt * 16 + (lane & 15), a.ldo / kTileK), num / den,
-             a.status);
+             bad);
   }
+  flush_range(a.status, bad);
 }
 
 static int g_attn_cus = 256;  // compute units of the device (set by attention_init)

@@ -50,7 +50,7 @@ __device__ __forceinline__ float silu(float z) {
 // the 16 lanes of a row together (sum of squares via shuffles).
 template <int EPI>
 __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool row_ok, int tile, int ln, float v,
-                                              float u, float rs, float h0, float sc, float gt) {
+                                              float u, float rs, float h0, float sc, float gt, unsigned &bad) {
   if (EPI == EPI_MOD) {
     // column c: layer c / 6d, part (c % 6d) / d (0..5 = a, b, g of the
     // attention norm, then of the MLP norm), index c % d; the final norm's
@@ -66,9 +66,9 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
         const int part = r6 / g.d_model, j = r6 - part * g.d_model;
         const int KBd = g.d_model / kTileK;
         if (part == 1 || part == 4)
-          store_op(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, j, KBd), mv, g.status);
+          store_op(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, j, KBd), mv, bad);
         else if (part == 0 && l == 0 && g.next)
-          store_op(g.next + afrag_index(row, j, KBd), g.h_in[(size_t)row * g.d_model + j] * (1.0f + mv), g.status);
+          store_op(g.next + afrag_index(row, j, KBd), g.h_in[(size_t)row * g.d_model + j] * (1.0f + mv), bad);
       }
     }
   } else if (EPI == EPI_RESID_F32) {
@@ -82,16 +82,16 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
     sq = sum_row16(sq);
     if (row_ok) {
       if ((ln & 15) == 0) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
-      if (g.mod_scale_next || g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * sc, g.status);
+      if (g.mod_scale_next || g.gain_next) store_op(g.next + afrag_index(row, col, g.N / kTileK), hv * sc, bad);
     }
   } else if (row_ok) {
     if (EPI == EPI_GEGLU) {
       const int col = (tile >> 1) * 16 + (ln & 15);
-      store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), gelu_tanh(v * rs) * (u * rs), g.status);
+      store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), gelu_tanh(v * rs) * (u * rs), bad);
     } else {
       const int col = tile * 16 + (ln & 15);
       if (EPI == EPI_BIAS_SILU) {
-        store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), silu(v + g.bias[col]), g.status);
+        store_op((op_t *)g.out + afrag_index(row, col, g.ldo / kTileK), silu(v + g.bias[col]), bad);
       } else if (EPI == EPI_QKV) {
         v *= rs;
         if (col < g.q_dim) {
@@ -297,6 +297,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
   // row 4*(lane>>4)+r, column lane&15.  The per-wave trip count is uniform and
   // the 16 lanes holding one row are always active together.
   const int n_out = n_out_all;
+  unsigned bad = 0;  // fp16 range flag of this thread's stores
   for (int e0 = 0, it = 0; e0 < n_out; e0 += blockDim.x, ++it) {
     const int e = e0 + threadIdx.x;
     if (e >= n_out) continue;  // whole waves only (n_out and blockDim are multiples of 64)
@@ -337,8 +338,9 @@ __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g) {
       }
     }
     const float rs = (!DUAL && kRstd && g.use_rstd && row_ok) ? rstd_s[rl] : 1.0f;
-    epilogue_elem<EPI>(g, row, row_ok, tile0 + t, ln, v, u, rs, h0, sc, gt);
+    epilogue_elem<EPI>(g, row, row_ok, tile0 + t, ln, v, u, rs, h0, sc, gt, bad);
   }
+  flush_range(g.status, bad);
 }
 
 template <int EPI, int T, int KPW>
@@ -422,9 +424,9 @@ __device__ __forceinline__ bool big_tile(const GemmArgs &g, int &mt0, int &nt0) 
 // TA*16 rows.
 __device__ __forceinline__ f32x4 ld4(const float *p) { return *(const f32x4 *)p; }
 __device__ __forceinline__ void st4(float *p, f32x4 v) { *(f32x4 *)p = v; }
-__device__ __forceinline__ void st4h(op_t *p, f32x4 v, unsigned *status) {
+__device__ __forceinline__ void st4h(op_t *p, f32x4 v, unsigned &bad) {
   *(f16x4 *)p = f16x4{(op_t)v[0], (op_t)v[1], (op_t)v[2], (op_t)v[3]};
-  check_op4(v[0], v[1], v[2], v[3], status);
+  check_op4(v[0], v[1], v[2], v[3], bad);
 }
 
 // Residual epilogue, store half, over NI row tiles starting at i0: h = h0 (or
@@ -435,7 +437,7 @@ template <int NI, bool ADA, int TA, int TB>
 __device__ __forceinline__ void big_resid_store(const GemmArgs &g, const f32x4 (&acc)[TA][TB], int i0, int mt, int nt,
                                                 int lane, const f32x4 (&h0)[NI][TB],
                                                 const f32x4 (&gt)[ADA ? NI : 1][TB],
-                                                const f32x4 (&sc)[ADA ? NI : 1][TB], bool has_next) {
+                                                const f32x4 (&sc)[ADA ? NI : 1][TB], bool has_next, unsigned &bad) {
   float *h = (float *)g.out;
   const int csub = 4 * (lane >> 4);
   const int KBn = g.N / kTileK;
@@ -452,7 +454,7 @@ __device__ __forceinline__ void big_resid_store(const GemmArgs &g, const f32x4 (
       sq = sum_pair32(sum_pair16(sq));  // the 4 lanes holding this row's 16 columns
       if (row_ok) {
         if (lane < 16) g.ssq[(size_t)tile * g.m_alloc + row] = sq;
-        if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ADA ? ii : 0][j], g.status);
+        if (has_next) st4h(g.next + afrag_index(row, col, KBn), hv * sc[ADA ? ii : 0][j], bad);
       }
     }
   }
@@ -498,27 +500,27 @@ __device__ __forceinline__ void big_resid_load(const GemmArgs &g, int i0, int mt
 // h0 loads of other rows, so the compiler would not hoist them).
 template <int NI, bool ADA, int TA, int TB>
 __device__ __forceinline__ void big_resid_rows(const GemmArgs &g, f32x4 (&acc)[TA][TB], int i0, int mt, int nt,
-                                               int lane) {
+                                               int lane, unsigned &bad) {
   f32x4 h0[NI][TB], gt[ADA ? NI : 1][TB], sc[ADA ? NI : 1][TB];
   big_resid_load<NI, ADA, TB>(g, i0, mt, nt, lane, h0, gt, sc);
   const bool has_next = ADA ? g.mod_scale_next != nullptr : g.gain_next != nullptr;
-  big_resid_store<NI, ADA, TA, TB>(g, acc, i0, mt, nt, lane, h0, gt, sc, has_next);
+  big_resid_store<NI, ADA, TA, TB>(g, acc, i0, mt, nt, lane, h0, gt, sc, has_next, bad);
 }
 
 template <int EPI, int TA, int TB, int I0 = 0, int NI = TA>
 __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA][TB], int mt, int nt, int lane,
-                                             const float *rstd) {
+                                             const float *rstd, unsigned &bad) {
   const int csub = 4 * (lane >> 4);
   if constexpr (EPI == EPI_RESID_F32) {
     if (g.mod_gate) {
 #pragma unroll
-      for (int i = I0; i < I0 + NI; ++i) big_resid_rows<1, true>(g, acc, i, mt, nt, lane);
+      for (int i = I0; i < I0 + NI; ++i) big_resid_rows<1, true>(g, acc, i, mt, nt, lane, bad);
     } else {
       // the whole tile in two halves: all of its h0 at once would cost the
       // main loop its second wave per SIMD (a half tile goes in one piece)
       constexpr int HB = NI == TA ? TA / 2 : NI;
 #pragma unroll
-      for (int i = I0; i < I0 + NI; i += HB) big_resid_rows<HB, false>(g, acc, i, mt, nt, lane);
+      for (int i = I0; i < I0 + NI; i += HB) big_resid_rows<HB, false>(g, acc, i, mt, nt, lane, bad);
     }
   } else if constexpr (EPI == EPI_QKV) {
     const int kvd = g.n_kv_heads * g.head_dim;
@@ -564,7 +566,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
         const f32x4 a = acc[i][j] * rs, u = acc[i][j + 1] * rs;
         st4h((op_t *)g.out + afrag_index(row, col, KBo),
              f32x4{gelu_tanh(a[0]) * u[0], gelu_tanh(a[1]) * u[1], gelu_tanh(a[2]) * u[2], gelu_tanh(a[3]) * u[3]},
-             g.status);
+             bad);
       }
     }
   } else if constexpr (EPI == EPI_BIAS_SILU) {
@@ -580,7 +582,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
       for (int j = 0; j < TB; ++j) {
         const f32x4 z = acc[i][j] + bias[j];
         st4h((op_t *)g.out + afrag_index(row, (nt + j) * 16 + csub, KBo),
-             f32x4{silu(z[0]), silu(z[1]), silu(z[2]), silu(z[3])}, g.status);
+             f32x4{silu(z[0]), silu(z[1]), silu(z[2]), silu(z[3])}, bad);
       }
     }
   } else if constexpr (EPI == EPI_MOD) {
@@ -606,10 +608,10 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
           const int part = r6 / g.d_model, jc = r6 - part * g.d_model;
           if (part == 1 || part == 4)
             st4h(g.mod_shift_ops + (size_t)(2 * l + (part == 4)) * g.shift_stride + afrag_index(row, jc, KBd), mv,
-                 g.status);
+                 bad);
           else if (part == 0 && l == 0 && g.next)
             st4h(g.next + afrag_index(row, jc, KBd), ld4(g.h_in + (size_t)row * g.d_model + jc) * (mv + 1.0f),
-                 g.status);
+                 bad);
         }
       }
     }
@@ -721,6 +723,7 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
     __syncthreads();
   }
 
+  unsigned bad = 0;  // fp16 range flag of this thread's stores
   if constexpr (DUAL) {
     // lane l of tile (i, j) holds row l & 15 (swapped operands)
 #pragma unroll
@@ -729,7 +732,7 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
 #pragma unroll
       for (int j = 0; j < TB; ++j) acc[i][j] = rs * acc[i][j] + acc2[i][j];
     }
-    big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, nullptr);
+    big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, nullptr, bad);
   } else if constexpr (KS == 2) {
     // Wave (wq, 0) keeps row tiles [0, H) and hands [H, TA) to wave (wq, 1),
     // which keeps [H, TA); each adds the other's partial of what it keeps.
@@ -755,18 +758,19 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
       for (int i = 0; i < H; ++i)
 #pragma unroll
         for (int j = 0; j < TB; ++j) acc[i][j] = acc[i][j] + other[(i * TB + j) * 64];
-      big_epilogue<EPI, TA, TB, 0, H>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, rs);
+      big_epilogue<EPI, TA, TB, 0, H>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, rs, bad);
     } else {
 #pragma unroll
       for (int i = 0; i < H; ++i)
 #pragma unroll
         for (int j = 0; j < TB; ++j) acc[H + i][j] = other[(i * TB + j) * 64] + acc[H + i][j];
-      big_epilogue<EPI, TA, TB, H, H>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, rs);
+      big_epilogue<EPI, TA, TB, H, H>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, rs, bad);
     }
   } else {
     big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane,
-                              (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr);
+                              (kRstd && g.use_rstd) ? rstd_s + wr * TA * 16 : nullptr, bad);
   }
+  flush_range(g.status, bad);
 }
 
 // LDS-ring kernels for the widest batched projections: RT x CT 16-row /
@@ -889,7 +893,10 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
     }
     __syncthreads();
   }
-  big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, g.use_rstd ? rstd_s + wr * TA * 16 : nullptr);
+  unsigned bad = 0;  // fp16 range flag of this thread's stores
+  big_epilogue<EPI, TA, TB>(g, acc, mt0 + wr * TA, nt0 + wc * TB, lane, g.use_rstd ? rstd_s + wr * TA * 16 : nullptr,
+                            bad);
+  flush_range(g.status, bad);
 }
 
 

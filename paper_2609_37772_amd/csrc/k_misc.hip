@@ -46,6 +46,7 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
   const int m0 = blockIdx.x * R;
   const int rows = load_action_rows<R>(x, M, Da, xs);
   const int KB = 2 * d / kTileK;
+  unsigned bad = 0;  // fp16 range flag of this thread's stores
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
   if (n < d) {
     float acc[R];
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
     }
 #pragma unroll
     for (int r = 0; r < R; ++r)
-      if (r < rows) store_op(te + afrag_index(m0 + r, n, KB), acc[r], status);
+      if (r < rows) store_op(te + afrag_index(m0 + r, n, KB), acc[r], bad);
   }
   const int half = d >> 1;
   if (n < half)
@@ -68,9 +69,10 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
       const float arg = freqs[n] * t[m0 + r];
       float sv, cv;
       sincosf(arg, &sv, &cv);  // one range reduction for both
-      store_op(te + afrag_index(m0 + r, d + n, KB), sv, status);
-      store_op(te + afrag_index(m0 + r, d + half + n, KB), cv, status);
+      store_op(te + afrag_index(m0 + r, d + n, KB), sv, bad);
+      store_op(te + afrag_index(m0 + r, d + half + n, KB), cv, bad);
     }
+  flush_range(status, bad);
 }
 
 // Adaptive-norm variant: te[m] = e(t_m) alone (K = d) as the time MLP's fp16
@@ -91,6 +93,7 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
   const int m0 = blockIdx.x * R;
   const int rows = load_action_rows<R>(x, M, Da, xs);
   const int KB = d / kTileK;
+  unsigned bad = 0;  // fp16 range flag of this thread's stores
   // d is a multiple of 32, so the 16 lanes of a 16-column tile are active together
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
   if (n < d) {
@@ -112,7 +115,7 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
       float sq = acc[r] * acc[r];
       sq = sum_row16(sq);
       if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
-      if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]), status);
+      if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]), bad);
     }
   }
   const int half = d >> 1;
@@ -121,9 +124,10 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
       const float arg = freqs[n] * t[m0 + r];
       float sv, cv;
       sincosf(arg, &sv, &cv);  // one range reduction for both
-      store_op(te + afrag_index(m0 + r, n, KB), sv, status);
-      store_op(te + afrag_index(m0 + r, half + n, KB), cv, status);
+      store_op(te + afrag_index(m0 + r, n, KB), sv, bad);
+      store_op(te + afrag_index(m0 + r, half + n, KB), cv, bad);
     }
+  flush_range(status, bad);
 }
 
 // v = RMSNorm(h) W_out^T + b_out, then x <- x + dt v unless frozen (mask or
@@ -358,8 +362,10 @@ __global__ __launch_bounds__(256) void time_feat_kernel(const float *__restrict_
   const int KB = d / kTileK;
   float sv, cv;
   sincosf(arg, &sv, &cv);  // one range reduction for both
-  store_op(te + afrag_index(r, n, KB), sv, status);
-  store_op(te + afrag_index(r, half + n, KB), cv, status);
+  unsigned bad = 0;
+  store_op(te + afrag_index(r, n, KB), sv, bad);
+  store_op(te + afrag_index(r, half + n, KB), cv, bad);
+  flush_range(status, bad);
 }
 
 hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps, int d, const float *freqs,

@@ -159,21 +159,6 @@ size_t attn_part_rows(const uad_ctx *c, int B, int H, int P) {
   return (size_t)sp * B * c->Hkv * rows_pad;
 }
 
-// Work of a context that owns its stream is ordered after everything the
-// caller queued on the null stream before the call, and the null stream's
-// later work after it (a caller-provided stream orders itself).
-hipError_t order_before(uad_ctx *c) {
-  if (!c->own_stream) return hipSuccess;
-  hipError_t e = hipEventRecord(c->ev_in, nullptr);
-  if (e == hipSuccess) e = hipStreamWaitEvent(c->stream, c->ev_in, 0);
-  return e;
-}
-hipError_t order_after(uad_ctx *c) {
-  if (!c->own_stream) return hipSuccess;
-  hipError_t e = hipEventRecord(c->ev_out, c->stream);
-  if (e == hipSuccess) e = hipStreamWaitEvent(nullptr, c->ev_out, 0);
-  return e;
-}
 
 // ---------------------------------------------------------------------------
 // Scratch of the no-allocation step (uad_denoise_step_static): the split-KV
@@ -265,16 +250,11 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->s_alloc = round_up(m.max_prefix + m.max_chunk, 32);
   c->layers.resize(c->L);
 
-  if (hip_stream) {
-    c->stream = (hipStream_t)hip_stream;
-  } else {
-    e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
-    if (e != hipSuccess) {
-      delete c;
-      return cerr(UAD_E_HIP, std::string("hipStreamCreate: ") + hipGetErrorString(e));
-    }
-    c->own_stream = true;
-  }
+  // the caller's stream; NULL is the device's null stream, so the library's
+  // work is ordered with the caller's other work there (a separate stream
+  // ordered by events around every call slowed the replayed step graphs by
+  // ~14% at batch 1)
+  c->stream = (hipStream_t)hip_stream;
   int rate_khz = 0;
   if (hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, device) == hipSuccess && rate_khz > 0)
     c->tick_hz = rate_khz * 1000.0;
@@ -414,8 +394,6 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->rel_stream, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_rel, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_out, hipEventDisableTiming);
   if (e != hipSuccess) {
     uad_destroy(c);
     return cerr(UAD_E_HIP, std::string("hipStreamCreate(capture/release): ") + hipGetErrorString(e));
@@ -446,9 +424,6 @@ void uad_destroy(uad_ctx *c) {
     (void)hipStreamDestroy(c->rel_stream);
   }
   if (c->ev_rel) (void)hipEventDestroy(c->ev_rel);
-  if (c->ev_in) (void)hipEventDestroy(c->ev_in);
-  if (c->ev_out) (void)hipEventDestroy(c->ev_out);
-  if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
 }
 
@@ -457,15 +432,7 @@ uad_status uad_set_stream(uad_ctx *c, void *hip_stream) {
   (void)hipSetDevice(c->device);
   hipError_t e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
-  if (hip_stream) {
-    if (c->own_stream) (void)hipStreamDestroy(c->stream);
-    c->own_stream = false;
-    c->stream = (hipStream_t)hip_stream;
-  } else if (!c->own_stream) {
-    e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
-    if (e != hipSuccess) return hip_fail(c, e, "hipStreamCreate");
-    c->own_stream = true;
-  }
+  c->stream = (hipStream_t)hip_stream;
   return UAD_OK;
 }
 
@@ -1104,17 +1071,6 @@ static uad_status run_work(uad_ctx *c, GraphKey k) {
   return UAD_OK;
 }
 
-// run_work between the null-stream ordering points of a library-owned stream.
-static uad_status run_ordered(uad_ctx *c, const GraphKey &k) {
-  hipError_t e = order_before(c);
-  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
-  uad_status rs = run_work(c, k);
-  if (rs != UAD_OK) return rs;
-  e = order_after(c);
-  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
-  return UAD_OK;
-}
-
 uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
                             float *v_out, int32_t batch, int32_t chunk) {
   if (!c) return UAD_E_INVALID;
@@ -1125,7 +1081,7 @@ uad_status uad_denoise_step(uad_ctx *c, float *x, const float *t, const float *d
   k.kind = 0;
   k.is_schedule = false;
   k.x = x; k.t = t; k.dt = dt; k.mask = mask; k.v_out = v_out; k.n_steps = 1; k.B = batch; k.H = chunk;
-  return run_ordered(c, k);
+  return run_work(c, k);
 }
 
 uad_status uad_denoise_step_static(uad_ctx *c, float *x, const float *t, const float *dt, const uint8_t *mask,
@@ -1148,15 +1104,9 @@ uad_status uad_denoise_step_static(uad_ctx *c, float *x, const float *t, const f
                                     " bytes of split-KV scratch; the static array holds " +
                                     std::to_string(kStaticScratchBytes));
   const StepScratch sc{(op_t *)base, (float *)(base + o_bytes)};
-  hipError_t e = order_before(c);
-  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
   // direct launches on the context stream: no graph capture or instantiation
-  st = enqueue_step(c, c->stream, x, t, dt, mask, nullptr, 0, 0, v_out, nullptr, nullptr, batch, chunk, nullptr, 0,
-                    nullptr, &sc);
-  if (st != UAD_OK) return st;
-  e = order_after(c);
-  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
-  return UAD_OK;
+  return enqueue_step(c, c->stream, x, t, dt, mask, nullptr, 0, 0, v_out, nullptr, nullptr, batch, chunk, nullptr, 0,
+                      nullptr, &sc);
 }
 
 uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, const float *dt_sched,
@@ -1173,7 +1123,7 @@ uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, cons
   k.is_schedule = true;
   k.x = x; k.t = t_sched; k.dt = dt_sched; k.mask = mask_sched; k.n_steps = n_steps; k.B = batch; k.H = chunk;
   k.released = released; k.release_step = release_step; k.step_ticks = step_ticks;
-  return run_ordered(c, k);
+  return run_work(c, k);
 }
 
 uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chunk, int32_t U, int32_t K,
@@ -1244,8 +1194,6 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
   k.x = x; k.B = batch; k.H = chunk; k.n_steps = Nstar; k.step_ticks = step_ticks;
   k.U = U; k.Kr = K; k.Nstar = Nstar; k.S = S; k.reconcile = reconcile;
   k.urgent = urgent_out; k.executed = executed_out; k.gac_mask = gac_mask; k.urgent_host = host_dev;
-  hipError_t oe = order_before(c);
-  if (oe != hipSuccess) return hip_fail(c, oe, "stream ordering");
   uad_status rs = run_work(c, k);
   if (rs != UAD_OK) return rs;
   // release: the urgent actions (and their pinned host copy) are final here;
@@ -1264,11 +1212,7 @@ uad_status uad_denoise_release(uad_ctx *c, float *x, int32_t batch, int32_t chun
   if (e != hipSuccess) return hip_fail(c, e, "uad_denoise_release: release");
   k.kind = 2;
   k.urgent_host = nullptr;
-  rs = run_work(c, k);
-  if (rs != UAD_OK) return rs;
-  e = order_after(c);
-  if (e != hipSuccess) return hip_fail(c, e, "stream ordering");
-  return UAD_OK;
+  return run_work(c, k);
 }
 
 uad_status uad_synchronize(uad_ctx *c) {

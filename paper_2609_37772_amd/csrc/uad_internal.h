@@ -66,15 +66,19 @@ __device__ __forceinline__ void raise_status(unsigned *status, unsigned bit) {
 
 // Every fp16 operand store checks its value: fp16 holds magnitudes below
 // 65520 (which round to at most 65504); anything larger becomes inf and a NaN
-// stays NaN, so both raise the context's range bit instead of passing silently.
-__device__ __forceinline__ void store_op(op_t *p, float v, unsigned *status) {
+// stays NaN.  The check is branch-free: a thread collects a flag over its
+// stores (`bad`) and raises the context's range bit once, at the end of its
+// kernel (flush_range), so the stores are issued as before.
+__device__ __forceinline__ void store_op(op_t *p, float v, unsigned &bad) {
   *p = (op_t)v;
-  if (!(__builtin_fabsf(v) < 65520.0f)) raise_status(status, kStatusRange);
+  bad |= (unsigned)!(__builtin_fabsf(v) < 65520.0f);
 }
-__device__ __forceinline__ void check_op4(float a, float b, float c, float d, unsigned *status) {
+__device__ __forceinline__ void check_op4(float a, float b, float c, float d, unsigned &bad) {
   const float T = 65520.0f;
-  const bool bad = !(__builtin_fabsf(a) < T) | !(__builtin_fabsf(b) < T) | !(__builtin_fabsf(c) < T) |
-                   !(__builtin_fabsf(d) < T);
+  bad |= (unsigned)(!(__builtin_fabsf(a) < T) | !(__builtin_fabsf(b) < T) | !(__builtin_fabsf(c) < T) |
+                    !(__builtin_fabsf(d) < T));
+}
+__device__ __forceinline__ void flush_range(unsigned *status, unsigned bad) {
   if (bad) raise_status(status, kStatusRange);
 }
 
@@ -336,8 +340,7 @@ struct uad_layer_ptrs {
 struct uad_ctx {
   uad_model_config cfg{};
   int device = 0;
-  hipStream_t stream = nullptr;
-  bool own_stream = false;
+  hipStream_t stream = nullptr;  // the caller's stream (null: the device's null stream)
   std::string err;
 
   int d = 0, L = 0, Hq = 0, Hkv = 0, hd = 0, F = 0, Da = 0;
@@ -395,7 +398,6 @@ struct uad_ctx {
   int tr_key[6] = {0, 0, 0, 0, 0, -1};         // B, H, U, K, N*, reconcile of the tables
   hipStream_t rel_stream = nullptr;            // release copies to pageable host memory
   hipEvent_t ev_rel = nullptr;
-  hipEvent_t ev_in = nullptr, ev_out = nullptr;  // null-stream ordering of a library-owned stream
   unsigned *status = nullptr;                  // device status word (kStatusRange, kStatusTimeout)
 
   // captured step / schedule graphs (small LRU cache)
