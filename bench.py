@@ -162,6 +162,48 @@ def summarize_counters(run_dir: str) -> dict:
     return out
 
 
+def summarize_mfma(run_dir: str) -> dict:
+    """MFMA busy and wave-state fractions per kernel from one rocprofv3 --pmc run
+    (SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE, SQ_WAVE_CYCLES, SQ_WAIT_ANY,
+    SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_ANY, SQ_INSTS_VALU_MFMA_MOPS_F16,
+    SQ_INSTS_VALU_MFMA_MOPS_BF16) found in DIR/pmc_mfma: MFMA busy = busy
+    cycles summed over SIMDs / (GPU active cycles x SIMDs), the counters'
+    own MfmaUtil expression; MFMA flops = (F16 + BF16 MOPS) x 512."""
+    import csv
+    import collections
+    rows = list(csv.DictReader(open(os.path.join(run_dir, "pmc_mfma", "run_counter_collection.csv"))))
+    simds = None
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    launches = collections.defaultdict(set)
+    for r in rows:
+        k = r["Kernel_Name"]
+        if "uad::" not in k or "stamp_kernel" in k:
+            continue
+        launches[k].add(r["Dispatch_Id"])
+        per[k][r["Counter_Name"]] += float(r["Counter_Value"])
+    agent = os.path.join(run_dir, "pmc_mfma", "run_agent_info.csv")
+    if os.path.exists(agent):
+        for r in csv.DictReader(open(agent)):
+            if r.get("Agent_Type") == "GPU" and int(r.get("Simd_Count", 0) or 0) > 0:
+                simds = int(r["Simd_Count"])
+    simds = simds or 1024
+    out = {"simds": simds, "kernels": {}}
+    for k, c in per.items():
+        wave = c.get("SQ_WAVE_CYCLES", 0.0) or 1.0
+        gui = c.get("GRBM_GUI_ACTIVE", 0.0) or 1.0
+        out["kernels"][k] = {
+            "launches": len(launches[k]),
+            "mfma_busy": round(c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui * simds), 4),
+            "wait_any": round(c.get("SQ_WAIT_ANY", 0.0) / wave, 4),
+            "wait_inst_any": round(c.get("SQ_WAIT_INST_ANY", 0.0) / wave, 4),
+            "active_inst_any": round(c.get("SQ_ACTIVE_INST_ANY", 0.0) / wave, 4),
+            "mfma_gflop_per_launch": round(512 * (c.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) +
+                                                  c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)) /
+                                           max(1, len(launches[k])) / 1e9, 3),
+        }
+    return out
+
+
 def measured_traffic(kernel_class: str):
     """Counter-measured bytes per launch of a class, if taken on the current sources; else None."""
     try:
@@ -426,12 +468,18 @@ def main():
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
                     help="print the per-launch traffic summary of two rocprofv3 --pmc runs found in DIR "
                          "(pmc_FETCH_SIZE/, pmc_WRITE_SIZE/) and exit; no GPU needed")
+    ap.add_argument("--summarize-mfma", metavar="DIR", default=None,
+                    help="print MFMA busy and wave-state fractions per kernel of a rocprofv3 --pmc run found in "
+                         "DIR/pmc_mfma and exit; no GPU needed")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy an MIB-MiB fp32 buffer 3 times (a plain copy kernel of known "
                          "size, the reference for hardware byte counters)")
     a = ap.parse_args()
     if a.summarize_counters:
         print(json.dumps(summarize_counters(a.summarize_counters), indent=1))
+        return
+    if a.summarize_mfma:
+        print(json.dumps(summarize_mfma(a.summarize_mfma), indent=1))
         return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the hot path is measured on one "
