@@ -434,11 +434,18 @@ def batched_leg(name, a, U, W, np, torch):
     torch.cuda.synchronize()
     log(f"[bench] {name}: set-up {time.time() - t0:.1f} s (inputs drawn on the device)")
     steps = max(a.steps, 20)
-    meas = measure(ex, wl, W.make_budgets(wl), noise, steps, a.warmup, min(a.sched_reps, 20), U, np, torch)
+    budgets = W.make_budgets(wl)
+    meas = measure(ex, wl, budgets, noise, steps, a.warmup, min(a.sched_reps, 20), U, np, torch)
+    comp = time_budget_schedules(ex, wl, budgets, noise, max(3, min(a.sched_reps, 20)), np, torch)
     ex.close()
     torch.cuda.empty_cache()
     fl = step_flops(wl)
     ms = meas["ms_per_step"]
+    # algorithmic work of a schedule: every environment for as many joint steps
+    # as its largest budget (a finished environment does no more work)
+    env_steps = int(budgets.max(axis=1).sum())
+    alg_flops = env_steps * fl / wl.batch
+    sched_ms = comp["median_ms"]
     return {"config": {"workload": name, "batch": wl.batch, "chunk": wl.chunk, "prefix": wl.prefix,
                        "layers": s.n_layers, "width": s.d_model,
                        "heads": f"{s.n_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.d_ff,
@@ -446,8 +453,44 @@ def batched_leg(name, a, U, W, np, torch):
             "ms_per_step": round(ms, 4), "env_steps_per_s": round(wl.batch * 1e3 / ms, 1),
             "steps": meas["steps"], "warmup": meas["warmup"],
             "flops_per_step": fl, "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
+            "note": "ms_per_step / mfma_frac: joint steps over all environments (uad_denoise_schedule)",
+            "schedule_from_budgets": {
+                "entry": "uad_denoise_budgets (environments whose tokens are all released are not evaluated)",
+                "median_ms": round(sched_ms, 4), "ci95_ms": comp["ci95_ms"], "schedules": comp["schedules"],
+                "joint_steps": int(meas["n"]), "active_envs_per_step": comp["active"],
+                "algorithmic_env_steps": env_steps, "algorithmic_flops": alg_flops,
+                "env_steps_per_s": round(env_steps / (sched_ms * 1e-3), 1),
+                "mfma_frac": round(alg_flops / (sched_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
+                "uncompacted_schedule_ms": meas["schedule_time"]["median_ms"]},
             "roofline": meas["roofline"], "kernels": meas["kernels"], "schedule_time": meas["schedule_time"],
             "data": "synthetic, drawn on the device (seeded torch generator, same distributions)"}
+
+
+def time_budget_schedules(ex, wl, budgets, noise, reps, np, torch):
+    """Device time of whole schedules run from budgets (finished environments
+    skipped), median and 95% bootstrap interval over reps schedules."""
+    n = int(budgets.max())
+    x0 = torch.from_numpy(noise).cuda()
+    x = torch.empty_like(x0)
+    hz = ex.tick_rate_hz()
+    ticks = torch.zeros(n + 1, dtype=torch.uint64).pin_memory()
+    x.copy_(x0)
+    ex.schedule_budgets(x, budgets)  # builds the graph
+    torch.cuda.synchronize()
+    per = []
+    for _ in range(reps):
+        x.copy_(x0)
+        ex.schedule_budgets(x, budgets, None, None, ticks)
+        torch.cuda.synchronize()
+        tk = ticks.numpy().astype(np.int64)
+        per.append((tk[-1] - tk[0]) / hz * 1e3)
+    per = np.array(per)
+    rng = np.random.default_rng(0)
+    boot = np.median(rng.choice(per, size=(8000, per.size), replace=True), axis=1)
+    active = [int(np.sum(budgets.max(axis=1) > k)) for k in range(n)]
+    log(f"[bench] {wl.name}: schedule from budgets median {np.median(per):.4f} ms (environments per step {active})")
+    return {"median_ms": float(np.median(per)), "schedules": int(per.size), "active": active,
+            "ci95_ms": [round(float(np.percentile(boot, 2.5)), 4), round(float(np.percentile(boot, 97.5)), 4)]}
 
 
 def main():

@@ -213,6 +213,26 @@ uad_status uad_denoise_schedule(uad_ctx *ctx, float *x, const float *t_sched, co
                                 const uint8_t *mask_sched, int32_t n_steps, int32_t batch, int32_t chunk,
                                 float *released, int32_t *release_step, uint64_t *step_ticks);
 
+/* A whole per-token schedule from integer budgets N_i (Sec. 4.2 Eqs. 4-5),
+ * with the step tables built by the library (as uad_build_schedule) and
+ * finished environments compacted away: joint step k evaluates only the
+ * environments that still have a token with N_i > k.  An environment whose
+ * tokens are all released takes no further part (the paper's per-token
+ * update leaves its states, released actions and release steps final), so
+ * the results are those of uad_denoise_schedule on the same tables, to
+ * rounding order (smaller steps may run other kernel variants).  The
+ * adaptive-norm expert evaluates every environment every step.
+ *   x                 device fp32 [batch][chunk][Da], in/out (x_0 in, final out)
+ *   budgets           host int32 [batch][chunk], each in 1..64; the tables are
+ *                     rebuilt and uploaded (waiting for the context's queued work)
+ *                     only when the budgets differ from the previous call's
+ *   released, release_step, step_ticks  as uad_denoise_schedule
+ *                     (step_ticks has max N_i + 1 entries)
+ * Errors: UAD_E_INVALID (null x/budgets, a budget outside 1..64), UAD_E_SHAPE,
+ * UAD_E_STATE, UAD_E_HIP. */
+uad_status uad_denoise_budgets(uad_ctx *ctx, float *x, const int32_t *budgets, int32_t batch, int32_t chunk,
+                               float *released, int32_t *release_step, uint64_t *step_ticks);
+
 /* Urgency-aware release of one chunk per environment (Sec. 4.2-4.4, App. C).
  * Tokens i < U are urgent: they take K steps of size 1/K while the tail takes
  * the canonical N* steps of 1/N*, all in ONE joint evaluation per step (N*

@@ -18,7 +18,7 @@ __all__ = [
     "LIB_PATH", "EXPORTED_SYMBOLS", "UadError", "load_library", "library_loaded",
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
     "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_step_static", "uad_denoise_schedule",
-    "uad_denoise_release", "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz",
+    "uad_denoise_budgets", "uad_denoise_release", "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz",
     "uad_debug_velocity_field", "uad_profile_enable", "uad_profile_read", "UAD_DTYPE_F32", "UAD_DTYPE_BF16", "STATUS_NAMES",
     "UAD_RELEASE_UAER", "UAD_RELEASE_TR", "UAD_FLAG_ADARMS",
 ]
@@ -31,7 +31,8 @@ STATUS_NAMES = {0: "UAD_OK", 1: "UAD_E_INVALID", 2: "UAD_E_SHAPE", 3: "UAD_E_STA
                 5: "UAD_E_HIP", 6: "UAD_E_OOM", 7: "UAD_E_UNSUPPORTED", 8: "UAD_E_RANGE"}
 EXPORTED_SYMBOLS = [
     "uad_create", "uad_destroy", "uad_last_error", "uad_set_stream", "uad_load_weights",
-    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_step_static", "uad_denoise_schedule", "uad_denoise_release",
+    "uad_set_prefix_kv", "uad_denoise_step", "uad_denoise_step_static", "uad_denoise_schedule", "uad_denoise_budgets",
+    "uad_denoise_release",
     "uad_build_schedule", "uad_aal", "uad_synchronize", "uad_tick_rate_hz", "uad_debug_velocity_field",
     "uad_profile_enable", "uad_profile_read",
 ]
@@ -77,6 +78,7 @@ def load_library() -> ctypes.CDLL:
         "uad_denoise_step": ([P, P, P, P, P, P, I32, I32], I32),
         "uad_denoise_step_static": ([P, P, P, P, P, P, I32, I32], I32),
         "uad_denoise_schedule": ([P, P, P, P, P, I32, I32, I32, P, P, P], I32),
+        "uad_denoise_budgets": ([P, P, P, I32, I32, P, P, P], I32),
         "uad_denoise_release": ([P, P, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P, P], I32),
         "uad_build_schedule": ([P, I32, I32, I32, P, P, P, P], I32),
         "uad_aal": ([P, I32, ctypes.c_double, P], I32),
@@ -260,6 +262,28 @@ def uad_denoise_schedule(ctx: int, x: torch.Tensor, t_sched: torch.Tensor, dt_sc
         tk = step_ticks.data_ptr()
     st = load_library().uad_denoise_schedule(ctx, *p, n, B, H, rel, rst, tk)
     _check(ctx, st, "uad_denoise_schedule")
+
+
+def uad_denoise_budgets(ctx: int, x: torch.Tensor, budgets: np.ndarray, released: Optional[torch.Tensor] = None,
+                        release_step: Optional[torch.Tensor] = None,
+                        step_ticks: Optional[torch.Tensor] = None) -> None:
+    """A schedule from host int budgets [B][H] (tables built by the library, finished environments skipped)."""
+    B, H, Da = x.shape
+    bud = np.ascontiguousarray(budgets, np.int32)
+    if bud.shape != (B, H):
+        raise ValueError(f"budgets must be [{B}][{H}], got {bud.shape}")
+    px = _dev_ptr(x, torch.float32, (B, H, Da), "x")
+    rel = _dev_ptr(released, torch.float32, (B, H, Da), "released")
+    rst = _dev_ptr(release_step, torch.int32, (B, H), "release_step")
+    tk = None
+    if step_ticks is not None:
+        n = int(bud.max())
+        if step_ticks.is_cuda or not step_ticks.is_pinned() or step_ticks.dtype != torch.uint64 \
+                or tuple(step_ticks.shape) != (n + 1,):
+            raise ValueError("step_ticks must be a pinned host uint64 tensor of max(budgets)+1 entries")
+        tk = step_ticks.data_ptr()
+    st = load_library().uad_denoise_budgets(ctx, px, bud.ctypes.data, B, H, rel, rst, tk)
+    _check(ctx, st, "uad_denoise_budgets")
 
 
 def uad_denoise_release(ctx: int, x: torch.Tensor, U: int, K: int, Nstar: int, S: int, mode: int,

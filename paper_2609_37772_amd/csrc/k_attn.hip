@@ -112,9 +112,11 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
   const int split = grp - eh * a.splits;
   const int b = eh / a.n_kv_heads;
   const int g = eh - b * a.n_kv_heads;
+  // K/V store slot of this environment (compacted steps run a subset)
+  const int ehkv = (a.env_map ? a.env_map[b] : b) * a.n_kv_heads + g;
 
-  const __bf16 *kbase = a.kc + (size_t)eh * a.s_alloc * HD;
-  const __bf16 *vbase = a.vtc + vt_index(eh, 0, 0, HD, a.s_alloc);
+  const __bf16 *kbase = a.kc + (size_t)ehkv * a.s_alloc * HD;
+  const __bf16 *vbase = a.vtc + vt_index(ehkv, 0, 0, HD, a.s_alloc);
 
   const int n_blocks = (a.n_keys + 31) / 32;
   const int blk0 = split * a.blocks_per_split;

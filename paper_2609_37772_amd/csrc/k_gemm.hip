@@ -98,12 +98,13 @@ __device__ __forceinline__ void epilogue_elem(const GemmArgs &g, int row, bool r
           ((__bf16 *)g.out)[(size_t)row * g.ldo + col] = (__bf16)v;
         } else {
           const int b = row / g.chunk, i = row - b * g.chunk;
+          const int bp = g.env_map ? g.env_map[b] : b;  // the environment's K/V store slot
           const int kvd = g.n_kv_heads * g.head_dim;
           const int c2 = col - g.q_dim;
           const bool is_v = c2 >= kvd;
           const int c3 = is_v ? c2 - kvd : c2;
           const int kvh = c3 / g.head_dim, c = c3 - kvh * g.head_dim;
-          const size_t env_head = (size_t)b * g.n_kv_heads + kvh;
+          const size_t env_head = (size_t)bp * g.n_kv_heads + kvh;
           const int s = g.prefix + i;
           if (!is_v)
             g.kc[(env_head * g.s_alloc + s) * g.head_dim + c] = (__bf16)v;
@@ -530,6 +531,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
       if (row >= g.M) continue;
       const float rs = rstd ? rstd[i * 16 + (lane & 15)] : 1.0f;
       const int b = row / g.chunk, s = g.prefix + (row - b * g.chunk);
+      const int bp = g.env_map ? g.env_map[b] : b;  // the environment's K/V store slot
 #pragma unroll
       for (int j = 0; j < TB; ++j) {
         const int col = (nt + j) * 16 + csub;
@@ -542,7 +544,7 @@ __device__ __forceinline__ void big_epilogue(const GemmArgs &g, f32x4 (&acc)[TA]
           const bool is_v = c2 >= kvd;
           const int c3 = is_v ? c2 - kvd : c2;
           const int kvh = c3 / g.head_dim, c = c3 - kvh * g.head_dim;
-          const size_t eh = (size_t)b * g.n_kv_heads + kvh;
+          const size_t eh = (size_t)bp * g.n_kv_heads + kvh;
           if (!is_v) {
             *(bf16x4 *)(g.kc + (eh * g.s_alloc + s) * g.head_dim + c) =
                 bf16x4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};

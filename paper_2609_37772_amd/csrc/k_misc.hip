@@ -19,13 +19,22 @@ __device__ __forceinline__ float block_sum_256(float v, float *scratch) {
 // Rows per workgroup of the embedding kernels: R tokens share one read of
 // their columns' W_in rows (R = 16 when batched: with one token per
 // workgroup the 3,200-token fleet re-read W_in 3,200 times from L2).
+// Token m of a compacted step is token env_map[m / chunk] * chunk + m % chunk
+// of the caller's arrays (null map: token m).
+__device__ __forceinline__ int phys_token(const int32_t *env_map, int chunk, int m) {
+  if (!env_map) return m;
+  const int b = m / chunk;
+  return env_map[b] * chunk + (m - b * chunk);
+}
+
 template <int R>
-__device__ __forceinline__ int load_action_rows(const float *__restrict__ x, int M, int Da, float (*xs)[64]) {
+__device__ __forceinline__ int load_action_rows(const float *__restrict__ x, int M, int Da, float (*xs)[64],
+                                                const int32_t *env_map = nullptr, int chunk = 1) {
   const int m0 = blockIdx.x * R;
   const int rows = min(R, M - m0);
   for (int i = threadIdx.x; i < rows * Da; i += blockDim.x) {
     const int r = i / Da, j = i - r * Da;
-    xs[r][j] = x[(size_t)(m0 + r) * Da + j];
+    xs[r][j] = x[(size_t)phys_token(env_map, chunk, m0 + r) * Da + j];
   }
   __syncthreads();
   return rows;
@@ -41,10 +50,10 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
                                                     int Da, int d, const float *__restrict__ w_in,
                                                     const float *__restrict__ b_in,
                                                     const float *__restrict__ freqs, op_t *__restrict__ te,
-                                                    unsigned *status) {
+                                                    unsigned *status, const int32_t *env_map, int chunk) {
   __shared__ float xs[R][64];
   const int m0 = blockIdx.x * R;
-  const int rows = load_action_rows<R>(x, M, Da, xs);
+  const int rows = load_action_rows<R>(x, M, Da, xs, env_map, chunk);
   const int KB = 2 * d / kTileK;
   unsigned bad = 0;  // fp16 range flag of this thread's stores
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
@@ -66,7 +75,7 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
   const int half = d >> 1;
   if (n < half)
     for (int r = 0; r < rows; ++r) {
-      const float arg = freqs[n] * t[m0 + r];
+      const float arg = freqs[n] * t[phys_token(env_map, chunk, m0 + r)];
       float sv, cv;
       sincosf(arg, &sv, &cv);  // one range reduction for both
       store_op(te + afrag_index(m0 + r, d + n, KB), sv, bad);
@@ -138,7 +147,8 @@ constexpr int kFinalOuts = 8;
 
 // Masked Euler update of token m, action dim a with velocity v (a copy when
 // frozen), the velocity outputs and the release bookkeeping.
-__device__ __forceinline__ void euler_out(const FinalArgs &f, int m, int a, float v) {
+__device__ __forceinline__ void euler_out(const FinalArgs &f, int mc, int a, float v) {
+  const int m = phys_token(f.env_map, f.chunk, mc);  // the caller's token of step row mc
   const size_t idx = (size_t)m * f.Da + a;
   const float dtm = f.dt[m];
   const bool frozen = (f.mask[m] != 0) || (dtm == 0.0f);
@@ -165,7 +175,8 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
   const int d = f.d;
   if (f.debug_field) {
     if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da)
-      vs[threadIdx.x] = f.dbg_alpha * f.x[(size_t)m * f.Da + a0 + threadIdx.x] + f.dbg_beta;
+      vs[threadIdx.x] = f.dbg_alpha * f.x[(size_t)phys_token(f.env_map, f.chunk, m) * f.Da + a0 + threadIdx.x] +
+                        f.dbg_beta;
   } else {
     const float *__restrict__ hr = f.h + (size_t)m * d;
     float hv[NC], gv[NC], sv[NC], wv[kFinalOuts][NC];
@@ -323,13 +334,14 @@ __global__ void stamp_kernel(uint64_t *dst) {
 
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                        const float *b_in, const float *freqs, op_t *te, unsigned *status, hipStream_t s,
-                       hipEvent_t ev0, hipEvent_t ev1) {
+                       hipEvent_t ev0, hipEvent_t ev1, const int32_t *env_map, int chunk) {
+  if (env_map && chunk < 1) return hipErrorInvalidValue;
   if (M >= 1024)
     UAD_LAUNCH(temb_kernel<16>, dim3((M + 15) / 16, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in,
-               b_in, freqs, te, status);
+               b_in, freqs, te, status, env_map, chunk);
   else
     UAD_LAUNCH(temb_kernel<1>, dim3(M, (d + 255) / 256), dim3(256), 0, s, ev0, ev1, x, t, M, Da, d, w_in, b_in, freqs,
-               te, status);
+               te, status, env_map, chunk);
   return hipGetLastError();
 }
 

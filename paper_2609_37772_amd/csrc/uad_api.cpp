@@ -355,7 +355,9 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
          o_trx0 = a.take<float>(M * Da), o_trv = a.take<float>(M * Da), o_trt = a.take<float>(kMaxTrSteps * M),
          o_trdt = a.take<float>(kMaxTrSteps * M), o_trm = a.take<uint8_t>(kMaxTrSteps * M),
          o_mod = a.take<float>(M * c->n_mod), o_mshift = a.take<uint16_t>(c->ada ? (size_t)2 * c->L * M * d : 0),
-         o_pf = a.take<unsigned>(64), o_status = a.take<unsigned>(1);
+         o_pf = a.take<unsigned>(64), o_status = a.take<unsigned>(1),
+         o_budt = a.take<float>(kMaxTrSteps * M), o_buddt = a.take<float>(kMaxTrSteps * M),
+         o_budm = a.take<uint8_t>(kMaxTrSteps * M), o_budmap = a.take<int32_t>((size_t)kMaxTrSteps * m.max_batch);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -382,6 +384,10 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->mod_shift_ops = (op_t *)(ab + o_mshift);
   c->pf_sink = (unsigned *)(ab + o_pf);
   c->status = (unsigned *)(ab + o_status);
+  c->bud_t = (float *)(ab + o_budt);
+  c->bud_dt = (float *)(ab + o_buddt);
+  c->bud_mask = (uint8_t *)(ab + o_budm);
+  c->bud_map = (int32_t *)(ab + o_budmap);
   e = attention_init();
   if (e == hipSuccess) e = gemm_init();
   // the no-allocation step's scratch: its address on this device (a failure is
@@ -684,7 +690,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
                                const uint8_t *mask, const uint8_t *next_mask, int is_last, int step, float *v_out,
                                float *released, int32_t *release_step, int B, int H, float *vsum = nullptr,
                                int vsum_tokens = 0, const AdaSlice *pre = nullptr,
-                               const StepScratch *scratch = nullptr) {
+                               const StepScratch *scratch = nullptr, const int32_t *env_map = nullptr) {
   const int M = B * H, d = c->d, F = c->F;
   const size_t MA = c->m_alloc;
   const bool prof = c->prof_on && !scratch;
@@ -710,7 +716,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     const int n_mod = c->n_mod;
     if (!c->ada) {
       UAD_CHECK_CLS(K_TEMB, launch_temb(x, t, M, c->Da, d, c->action_in_w, c->action_in_b, c->freqs, c->a_te, c->status, s,
-                                        ea_, eb_));
+                                        ea_, eb_, env_map, H));
       GemmArgs g{};
       g.status = c->status;
       g.M = M; g.m_alloc = (int)MA;
@@ -755,6 +761,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
 
     AttnArgs at{};
     at.status = c->status;
+    at.env_map = env_map;
     at.q = c->q; at.ldq = c->q_dim; at.s_alloc = c->s_alloc; at.n_keys = c->prefix_len + H;
     at.chunk = H; at.n_heads = c->Hq; at.n_kv_heads = c->Hkv; at.group = c->Hq / c->Hkv;
     at.rows = at.group * H; at.rows_pad = (at.rows + 63) / 64 * 64;
@@ -788,6 +795,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       q.M = M; q.A = c->a_n; q.W = lp.wqkv; q.N = c->n_qkv; q.K = d;
       q.out = c->q; q.ldo = c->q_dim; q.kc = kc; q.vtc = vtc; q.chunk = H; q.prefix = c->prefix_len;
       q.s_alloc = c->s_alloc; q.n_kv_heads = c->Hkv; q.head_dim = c->hd; q.q_dim = c->q_dim;
+      q.env_map = env_map;
       norm_fields(q); q.use_rstd = 1;
       const float *mod_base = pre ? pre->mod : c->mod;
       const op_t *shift_base = pre ? pre->shift : c->mod_shift_ops;
@@ -846,7 +854,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
   f.M = M; f.d = d; f.Da = c->Da; f.x = x; f.t = t; f.dt = dt; f.mask = mask; f.next_mask = next_mask;
   f.is_last_step = is_last; f.step = step; f.v_out = v_out; f.released = released; f.release_step = release_step;
   f.debug_field = c->dbg ? 1 : 0; f.dbg_alpha = c->dbg_alpha; f.dbg_beta = c->dbg_beta;
-  f.vsum = vsum; f.vsum_tokens = vsum_tokens; f.chunk = H;
+  f.vsum = vsum; f.vsum_tokens = vsum_tokens; f.chunk = H; f.env_map = env_map;
   if (c->ada) {
     f.mod_scale = (pre ? pre->mod : c->mod) + (size_t)c->L * 6 * d; f.mod_shift = f.mod_scale + d;
     f.mod_ld = c->n_mod;
@@ -1017,7 +1025,31 @@ static uad_status enqueue_release_phase(uad_ctx *c, hipStream_t s, const GraphKe
   return UAD_OK;
 }
 
+// A schedule from budgets (uad_denoise_budgets) on stream s: at step k only
+// the k.active[k] environments that still have an active token are evaluated,
+// their ascending list at bud_map + k * max_batch; the step tables are the
+// library's own (bud_t, bud_dt, bud_mask, [n_steps][B][H]).
+static uad_status enqueue_budgets(uad_ctx *c, hipStream_t s, const GraphKey &k) {
+  const size_t M = (size_t)k.B * k.H;
+  hipError_t e = hipSuccess;
+  if (k.step_ticks && (e = launch_stamp(k.step_ticks, s)) != hipSuccess) return hip_fail(c, e, "launch_stamp");
+  for (int st = 0; st < k.n_steps; ++st) {
+    const bool last = st == k.n_steps - 1;
+    const uint8_t *next = last ? nullptr : c->bud_mask + (st + 1) * M;
+    const int Bk = k.active[st];
+    const int32_t *map = Bk < k.B ? c->bud_map + (size_t)st * c->cfg.max_batch : nullptr;
+    uad_status rs = enqueue_step(c, s, k.x, c->bud_t + st * M, c->bud_dt + st * M, c->bud_mask + st * M, next,
+                                 last ? 1 : 0, st, nullptr, k.released, k.release_step, Bk, k.H, nullptr, 0, nullptr,
+                                 nullptr, map);
+    if (rs != UAD_OK) return rs;
+    if (k.step_ticks && (e = launch_stamp(k.step_ticks + st + 1, s)) != hipSuccess)
+      return hip_fail(c, e, "launch_stamp");
+  }
+  return UAD_OK;
+}
+
 static uad_status enqueue_work(uad_ctx *c, hipStream_t s, const GraphKey &k) {
+  if (k.kind == 3) return enqueue_budgets(c, s, k);
   return k.kind == 0 ? enqueue_schedule(c, s, k) : enqueue_release_phase(c, s, k);
 }
 
@@ -1123,6 +1155,67 @@ uad_status uad_denoise_schedule(uad_ctx *c, float *x, const float *t_sched, cons
   k.is_schedule = true;
   k.x = x; k.t = t_sched; k.dt = dt_sched; k.mask = mask_sched; k.n_steps = n_steps; k.B = batch; k.H = chunk;
   k.released = released; k.release_step = release_step; k.step_ticks = step_ticks;
+  return run_work(c, k);
+}
+
+uad_status uad_denoise_budgets(uad_ctx *c, float *x, const int32_t *budgets, int32_t batch, int32_t chunk,
+                               float *released, int32_t *release_step, uint64_t *step_ticks) {
+  if (!c) return UAD_E_INVALID;
+  const std::string fn = "uad_denoise_budgets";
+  if (!x || !budgets) return fail(c, UAD_E_INVALID, fn + ": null x/budgets");
+  if (batch < 1 || chunk < 1) return fail(c, UAD_E_INVALID, fn + ": batch and chunk must be >= 1");
+  if (batch > c->cfg.max_batch || chunk > c->cfg.max_chunk)
+    return fail(c, UAD_E_SHAPE, fn + ": batch/chunk beyond the context maxima");
+  if (!c->dbg) {
+    if (!c->weights_loaded) return fail(c, UAD_E_STATE, fn + ": weights not loaded");
+    if (!c->prefix_set) return fail(c, UAD_E_STATE, fn + ": prefix K/V not set");
+    if (batch > c->prefix_batch) return fail(c, UAD_E_STATE, fn + ": prefix set for fewer environments");
+  }
+  (void)hipSetDevice(c->device);
+  const size_t M = (size_t)batch * chunk;
+  // tables and per-step environment lists, rebuilt when the budgets change
+  std::vector<int32_t> key;
+  key.reserve(2 + M);
+  key.push_back(batch);
+  key.push_back(chunk);
+  key.insert(key.end(), budgets, budgets + M);
+  if (key != c->bud_key) {
+    std::vector<float> t(kMaxTrSteps * M), dt(kMaxTrSteps * M);
+    std::vector<uint8_t> mk(kMaxTrSteps * M);
+    int32_t n = 0;
+    std::string err;
+    if (!build_schedule_host(budgets, batch, chunk, kMaxTrSteps, &n, t.data(), dt.data(), mk.data(), &err))
+      return fail(c, UAD_E_INVALID, fn + ": " + err + " (budgets must lie in 1..64)");
+    // environment b has an active token at step k while its largest budget exceeds k
+    const int maxb = c->cfg.max_batch;
+    std::vector<int32_t> map((size_t)n * maxb, 0);
+    std::vector<uint16_t> act(n);
+    for (int k = 0; k < n; ++k) {
+      int cnt = 0;
+      for (int b = 0; b < batch; ++b) {
+        int nb = 0;
+        for (int i = 0; i < chunk; ++i) nb = std::max(nb, budgets[(size_t)b * chunk + i]);
+        if (nb > k || c->ada) map[(size_t)k * maxb + cnt++] = b;  // adaptive norm: every environment
+      }
+      act[k] = (uint16_t)cnt;
+    }
+    hipError_t e = hipStreamSynchronize(c->stream);  // queued work may read the previous tables
+    if (e == hipSuccess) e = hipMemcpy(c->bud_t, t.data(), n * M * sizeof(float), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(c->bud_dt, dt.data(), n * M * sizeof(float), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(c->bud_mask, mk.data(), n * M, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(c->bud_map, map.data(), map.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      c->bud_key.clear();
+      return hip_fail(c, e, "uad_denoise_budgets: step tables");
+    }
+    c->bud_key = key;
+    c->bud_active = act;
+  }
+  GraphKey k{};
+  k.kind = 3;
+  k.x = x; k.B = batch; k.H = chunk; k.n_steps = (int)c->bud_active.size();
+  k.released = released; k.release_step = release_step; k.step_ticks = step_ticks;
+  for (int i = 0; i < k.n_steps; ++i) k.active[i] = c->bud_active[i];
   return run_work(c, k);
 }
 

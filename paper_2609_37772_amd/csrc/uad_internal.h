@@ -192,6 +192,9 @@ struct GemmArgs {
   __bf16 *vtc;  // layer V^T store, 32-key blocks (vt_index)
   int chunk, prefix, s_alloc, n_kv_heads, head_dim, q_dim;
   unsigned *status;  // context status word (range bit of the fp16 operand stores)
+  // compacted steps: environment j of this step is environment env_map[j] of
+  // the caller's batch (its K/V store slot); null when every environment runs
+  const int32_t *env_map;
 };
 
 // Up to two byte ranges (weights of the next projections) that otherwise idle
@@ -222,6 +225,7 @@ struct AttnArgs {
   Prefetch pre_comb;  // read by an extra slice of the split-merge grid (wgs: nonzero = on)
   unsigned *pf_sink;  // one word the prefetch may write (keeps its loads alive)
   unsigned *status;   // context status word (range bit of the fp16 stores)
+  const int32_t *env_map;  // compacted steps: K/V store environment of each environment of the step, or null
 };
 
 struct FinalArgs {
@@ -248,6 +252,9 @@ struct FinalArgs {
   // Trajectory Reconciliation: vsum[m] += v for tokens (m % chunk) < vsum_tokens
   float *vsum;          // [M][Da] or null
   int vsum_tokens, chunk;
+  // compacted steps: token m of the step (h row m) is token
+  // env_map[m / chunk] * chunk + m % chunk of x, t, dt, masks and outputs
+  const int32_t *env_map;
 };
 
 // Urgency-aware release with Trajectory Reconciliation and Ghost Action
@@ -279,9 +286,12 @@ hipError_t attention_init();             // once per context: raise the kernels'
 hipError_t gemm_init();                  // once per context: raise the batched GEMM's LDS limit
 int attention_chunk_blocks(int head_dim);  // 32-key blocks loaded per round trip
 int attention_max_splits(int head_dim);    // split-KV partials the combine accepts
+// env_map (compacted steps): token m of the step reads x and t of token
+// env_map[m / chunk] * chunk + m % chunk (null: token m)
 hipError_t launch_temb(const float *x, const float *t, int M, int Da, int d, const float *w_in,
                        const float *b_in, const float *freqs, op_t *te, unsigned *status, hipStream_t s,
-                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr, const int32_t *env_map = nullptr,
+                       int chunk = 1);
 // adaptive-norm variant: te <- e(t) (K = d); h <- W_in x + b_in with its
 // per-16-column sums of squares ssq[d/16][m_alloc]
 hipError_t launch_temb_ada(const float *x, const float *t, int M, int Da, int d, const float *w_in,
@@ -308,7 +318,8 @@ bool build_schedule_host(const int32_t *budgets, int batch, int chunk, int max_s
 // ---------------------------------------------------------------------------
 // Everything a captured step/schedule graph depends on.
 struct GraphKey {
-  int kind;  // 0: step / schedule; 1, 2: urgency-aware release phases before / after the release
+  int kind;  // 0: step / schedule; 1, 2: urgency-aware release phases before / after the release;
+             // 3: schedule from budgets with finished environments compacted away
   bool is_schedule;
   float *x;
   const float *t, *dt;
@@ -322,7 +333,11 @@ struct GraphKey {
   float *urgent, *executed;
   const uint8_t *gac_mask;
   float *urgent_host;  // device address of the pinned host copy written by the release kernel, or null
+  // kind 3: environments evaluated at each step (their list is device data the graph reads)
+  uint16_t active[uad::kMaxTrSteps];
   bool operator==(const GraphKey &o) const {
+    for (int i = 0; i < uad::kMaxTrSteps; ++i)
+      if (active[i] != o.active[i]) return false;
     return kind == o.kind && U == o.U && Kr == o.Kr && Nstar == o.Nstar && S == o.S && reconcile == o.reconcile &&
            urgent == o.urgent && executed == o.executed && gac_mask == o.gac_mask && urgent_host == o.urgent_host &&
            is_schedule == o.is_schedule && x == o.x && t == o.t && dt == o.dt && mask == o.mask &&
@@ -396,6 +411,13 @@ struct uad_ctx {
   float *tr_t = nullptr, *tr_dt = nullptr;     // [kMaxSteps][m_alloc] step tables of the last configuration
   uint8_t *tr_mask = nullptr;
   int tr_key[6] = {0, 0, 0, 0, 0, -1};         // B, H, U, K, N*, reconcile of the tables
+  // schedules from budgets (uad_denoise_budgets): step tables, and per step the
+  // ascending list of environments with an active token, for the last budgets
+  float *bud_t = nullptr, *bud_dt = nullptr;   // [kMaxTrSteps][m_alloc]
+  uint8_t *bud_mask = nullptr;
+  int32_t *bud_map = nullptr;                  // [kMaxTrSteps][max_batch]
+  std::vector<int32_t> bud_key;                // budgets of the uploaded tables (B, H, then B*H budgets)
+  std::vector<uint16_t> bud_active;            // environments per step
   hipStream_t rel_stream = nullptr;            // release copies to pageable host memory
   hipEvent_t ev_rel = nullptr;
   unsigned *status = nullptr;                  // device status word (kStatusRange, kStatusTimeout)

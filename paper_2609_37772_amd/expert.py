@@ -42,6 +42,10 @@ class ActionExpert:
     def schedule(self, x, t_sched, dt_sched, mask_sched, released=None, release_step=None, step_ticks=None):
         B.uad_denoise_schedule(self.ctx, x, t_sched, dt_sched, mask_sched, released, release_step, step_ticks)
 
+    def schedule_budgets(self, x, budgets, released=None, release_step=None, step_ticks=None):
+        """A schedule from host budgets, finished environments skipped (uad_denoise_budgets)."""
+        B.uad_denoise_budgets(self.ctx, x, budgets, released, release_step, step_ticks)
+
     def release(self, x, U: int, K: int, Nstar: int, S: int, reconcile: bool = True, urgent=None,
                 executed=None, gac_mask=None, urgent_host=None, release_event=None, step_ticks=None):
         """Urgency-aware release (UAER, or TR + ghosts, GAC when ``executed`` is given).

@@ -89,14 +89,33 @@ def _steps_to_force(n):
     return sorted({0, n // 2, n - 1})
 
 
+_oracle_runs = {}
+
+
+def oracle_schedule(c, tag):
+    """The oracle's schedule of every environment of case c (with history), computed once per case."""
+    if tag not in _oracle_runs:
+        log(f"[{tag}] oracle schedule of {c.wl.batch} environments")
+        _oracle_runs[tag] = O.denoise_schedule(c.oracle_model(), c.noise, c.budgets, keep_history=True)
+    return _oracle_runs[tag]
+
+
+def run_budgets_gpu(c, x0, budgets):
+    xg = dev(x0.astype(np.float32))
+    rel = torch.zeros_like(xg)
+    rst = torch.full(budgets.shape, -1, dtype=torch.int32, device="cuda")
+    c.expert.schedule_budgets(xg, budgets, rel, rst)
+    c.expert.synchronize()
+    return xg.cpu().numpy(), rel.cpu().numpy(), rst.cpu().numpy()
+
+
 def _every_env_against_oracle(c, tag):
     """Every environment of a batched workload against the oracle: per-step
     velocities teacher-forced at the first, a middle and the last step (the
     GPU step gets the oracle's states of ALL environments), then the
     free-running schedule's released actions, final states and release steps."""
     B = c.wl.batch
-    log(f"[{tag}] oracle schedule of {B} environments")
-    r = O.denoise_schedule(c.oracle_model(), c.noise, c.budgets, keep_history=True)
+    r = oracle_schedule(c, tag)
     worst_v = 0.0
     for k in _steps_to_force(r["n_steps"]):
         x_in, v_ref = r["history"][k]
@@ -126,6 +145,58 @@ def test_fleet_every_env(gpu):
 def test_large_every_env(gpu):
     """24 layers, width 1536, GQA 12/2, H=128, 16 environments, linear budgets 3..12."""
     _every_env_against_oracle(case("large_b16"), "large")
+
+
+@pytest.mark.timeout(900)
+def test_fleet_budgets_finished_environments_skipped(gpu):
+    """uad_denoise_budgets on the fleet (per-environment budgets 3..10): steps
+    after an environment's last release skip it; every environment's released
+    actions, final states and release steps against the oracle, and against
+    the uncompacted schedule on the same tables."""
+    c = case("pi0_fleet_b64")
+    r = oracle_schedule(c, "fleet")
+    x, rel, rst = run_budgets_gpu(c, c.noise, c.budgets)
+    xs, rels, rsts = run_schedule_gpu(c, c.noise, c.budgets)
+    err_rel = float(np.max(np.abs(rel - r["released"])))
+    err_x = float(np.max(np.abs(x - r["x"])))
+    err_vs = float(np.max(np.abs(rel - rels)))
+    active = [int(np.sum(c.budgets.max(axis=1) > k)) for k in range(r["n_steps"])]
+    log(f"[fleet budgets] environments per step {active}; released max abs err {err_rel:.2e}, "
+        f"final {err_x:.2e}; vs uncompacted schedule {err_vs:.2e}")
+    assert err_rel <= ACT_ATOL and err_x <= ACT_ATOL and err_vs <= ACT_ATOL
+    np.testing.assert_array_equal(rst, r["release_step"])
+    np.testing.assert_array_equal(rst, rsts)
+    assert rel.tobytes() == x.tobytes()
+
+
+def test_budgets_non_contiguous_finished_environments(gpu):
+    """Four environments finishing at steps 3, 1, 5 and 2 (largest budgets), so
+    the environments still running are not a prefix of the batch: against the
+    oracle, and under the linear field v = alpha x + beta bit for bit against
+    the uncompacted schedule and within 2e-6 of the closed form."""
+    c = case("tiny", batch=4)
+    H = c.wl.chunk
+    bud = np.stack([np.full(H, 3), np.full(H, 1), np.array([1 + (i % 5) for i in range(H)]),
+                    np.array([1 + (i % 2) for i in range(H)])]).astype(np.int32)
+    r = O.denoise_schedule(c.oracle_model(), c.noise, bud)
+    x, rel, rst = run_budgets_gpu(c, c.noise, bud)
+    e = float(np.max(np.abs(rel - r["released"])))
+    log(f"[budgets, 4 environments] released max abs err {e:.2e}")
+    assert e <= ACT_ATOL and float(np.max(np.abs(x - r["x"]))) <= ACT_ATOL
+    np.testing.assert_array_equal(rst, r["release_step"])
+    alpha, beta = 0.35, -0.2
+    c.expert.debug_velocity_field(True, alpha, beta)
+    try:
+        xb, relb, rstb = run_budgets_gpu(c, c.noise, bud)
+        xs, rels, rsts = run_schedule_gpu(c, c.noise, bud)
+    finally:
+        c.expert.debug_velocity_field(False)
+    assert relb.tobytes() == rels.tobytes() and xb.tobytes() == xs.tobytes()
+    np.testing.assert_array_equal(rstb, rsts)
+    N = bud.astype(np.float64)[..., None]
+    g = (1.0 + alpha * (-1.0 / N)) ** N
+    ref = g * c.noise + beta * (g - 1.0) / alpha
+    np.testing.assert_allclose(relb, ref, rtol=2e-6, atol=2e-6)
 
 
 def test_frozen_tokens_bit_identical_batched(gpu):
