@@ -168,7 +168,9 @@ def summarize_mfma(run_dir: str) -> dict:
     SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_ANY, SQ_INSTS_VALU_MFMA_MOPS_F16,
     SQ_INSTS_VALU_MFMA_MOPS_BF16) found in DIR/pmc_mfma: MFMA busy = busy
     cycles summed over SIMDs / (GPU active cycles x SIMDs), the counters'
-    own MfmaUtil expression; MFMA flops = (F16 + BF16 MOPS) x 512."""
+    own MfmaUtil expression, whose GPU active cycles are those of one XCC (the
+    CSV sums them over the XCCs, so they are divided by their number); MFMA
+    flops = (F16 + BF16 MOPS) x 512."""
     import csv
     import collections
     rows = list(csv.DictReader(open(os.path.join(run_dir, "pmc_mfma", "run_counter_collection.csv"))))
@@ -182,15 +184,18 @@ def summarize_mfma(run_dir: str) -> dict:
         launches[k].add(r["Dispatch_Id"])
         per[k][r["Counter_Name"]] += float(r["Counter_Value"])
     agent = os.path.join(run_dir, "pmc_mfma", "run_agent_info.csv")
+    xcc = None
     if os.path.exists(agent):
         for r in csv.DictReader(open(agent)):
             if r.get("Agent_Type") == "GPU" and int(r.get("Simd_Count", 0) or 0) > 0:
                 simds = int(r["Simd_Count"])
+                xcc = int(r.get("Num_Xcc", 0) or 0) or None
     simds = simds or 1024
-    out = {"simds": simds, "kernels": {}}
+    xcc = xcc or 8
+    out = {"simds": simds, "xcc": xcc, "kernels": {}}
     for k, c in per.items():
         wave = c.get("SQ_WAVE_CYCLES", 0.0) or 1.0
-        gui = c.get("GRBM_GUI_ACTIVE", 0.0) or 1.0
+        gui = (c.get("GRBM_GUI_ACTIVE", 0.0) / xcc) or 1.0
         out["kernels"][k] = {
             "launches": len(launches[k]),
             "mfma_busy": round(c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui * simds), 4),
