@@ -209,6 +209,67 @@ def summarize_mfma(run_dir: str) -> dict:
     return out
 
 
+STEP_ROLES = ("qkv", "attention", "combine", "o", "gateup", "down")
+
+
+def summarize_timeline(run_dir: str, workload: str = "pi0_b1") -> dict:
+    """Per-layer timeline of the replayed step graphs of a rocprofv3 --kernel-trace run
+    (DIR/run_kernel_trace.csv). A step is the run of kernels from the time embedding to the
+    final Euler kernel: 3 + 6 per layer + 1. Only steps whose kernels ran back to back (gaps
+    summing to under 2 us) are kept: the profiler stretches the others. For each position:
+    mean duration, mean gap before it, and the time its algorithmic bytes need at HBM peak."""
+    import csv
+    import statistics
+    import uad_workloads as W
+    wl = W.get_workload(workload)
+    L = wl.shape.n_layers
+    rows = list(csv.DictReader(open(os.path.join(run_dir, "run_kernel_trace.csv"))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    want = (["temb_kernel", "gemm_kernel<0,", "gemm_kernel<1,"] +
+            ["gemm_kernel<4,", "attn_kernel<", "attn_combine_kernel", "gemm_kernel<1,", "gemm_kernel<3,",
+             "gemm_kernel<1,"] * L + ["final_kernel"])
+    steps, cur = [], None
+    for r in rows:
+        k = r["Kernel_Name"]
+        if ("uad::" not in k and "_ZN3uad" not in k) or "stamp_kernel" in k:
+            continue
+        if "temb_kernel" in k:
+            cur = []
+        if cur is None:
+            continue
+        cur.append((k, int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+        if "final_kernel" in k:
+            if len(cur) == len(want) and all(w in n for w, (n, _, _) in zip(want, cur)):
+                steps.append(cur)
+            cur = None
+    tight = [s for s in steps if sum(max(0, s[i][1] - s[i - 1][2]) for i in range(1, len(s))) < 2000]
+    if not tight:
+        raise SystemExit("no back-to-back steps in the trace")
+    dur = [statistics.mean((s[i][2] - s[i][1]) / 1e3 for s in tight) for i in range(len(want))]
+    gap = [0.0] + [statistics.mean((s[i][1] - s[i - 1][2]) / 1e3 for s in tight) for i in range(1, len(want))]
+    kb = kernel_bytes(wl, wl.batch * wl.chunk)
+    role_bytes = {"qkv": kb["gemm_qkv"], "attention": kb["attention"], "combine": 0, "o": kb["gemm_o"],
+                  "gateup": kb["gemm_gateup"], "down": kb["gemm_down"]}
+    layers = []
+    for l in range(L):
+        base = 3 + 6 * l
+        layers.append({"layer": l, "busy_us": round(sum(dur[base:base + 6]), 2),
+                       "gaps_us": round(sum(gap[base:base + 6]), 2),
+                       "kernels_us": {r: round(dur[base + j], 2) for j, r in enumerate(STEP_ROLES)}})
+    per_role = {r: round(statistics.mean(dur[3 + 6 * l + j] for l in range(L)), 2) for j, r in enumerate(STEP_ROLES)}
+    return {
+        "workload": workload, "steps_in_trace": len(steps), "back_to_back_steps": len(tight),
+        "step_span_us": round(statistics.mean((s[-1][2] - s[0][1]) / 1e3 for s in tight), 2),
+        "prologue_us": {"temb": round(dur[0], 2), "time_in": round(dur[1], 2), "time_out": round(dur[2], 2)},
+        "final_us": round(dur[-1], 2),
+        "gaps_total_us": round(sum(gap), 2),
+        "layer_mean_us": per_role | {"total": round(sum(per_role.values()), 2)},
+        "layer_bytes": role_bytes,
+        "layer_bytes_us_at_peak": {r: round(b / (HBM_PEAK_GBS * 1e3), 2) for r, b in role_bytes.items()},
+        "layers": layers,
+    }
+
+
 def measured_traffic(kernel_class: str):
     """Counter-measured bytes per launch of a class, if taken on the current sources; else None."""
     try:
@@ -519,6 +580,9 @@ def main():
     ap.add_argument("--summarize-mfma", metavar="DIR", default=None,
                     help="print MFMA busy and wave-state fractions per kernel of a rocprofv3 --pmc run found in "
                          "DIR/pmc_mfma and exit; no GPU needed")
+    ap.add_argument("--summarize-timeline", metavar="DIR", default=None,
+                    help="print the per-layer timeline of the replayed step graphs in a rocprofv3 --kernel-trace "
+                         "run found in DIR (run_kernel_trace.csv) and exit; no GPU needed")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy an MIB-MiB fp32 buffer 3 times (a plain copy kernel of known "
                          "size, the reference for hardware byte counters)")
@@ -528,6 +592,9 @@ def main():
         return
     if a.summarize_mfma:
         print(json.dumps(summarize_mfma(a.summarize_mfma), indent=1))
+        return
+    if a.summarize_timeline:
+        print(json.dumps(summarize_timeline(a.summarize_timeline, a.workload), indent=1))
         return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the hot path is measured on one "
