@@ -49,6 +49,15 @@ constexpr int attn_chunk_blocks() {
   return HD == 256 ? 2 : 4;
 }
 
+// Blocks per stage of the tall batched workgroups (6-8 waves): the waves
+// meet once per stage.  Same-box A/B per launch: HD = 128 (2048 tokens x 1152
+// keys) 33.2 -> 32.4 us with 2 blocks (4 blocks: 33.2); HD = 256 (3200 tokens x
+// 866 keys) 45.3 -> 46.2 us with 2, so one there.
+template <int HD>
+constexpr int attn_tall_blocks() {
+  return HD == 256 ? 1 : 2;
+}
+
 typedef __attribute__((address_space(3))) void lds_void;
 
 
@@ -415,12 +424,14 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
       AttnArgs at = a;
       at.qblocks = (a.rows + 16 * best_nw - 1) / (16 * best_nw);
       const dim3 g2(8 * ((groups + 7) / 8) * at.qblocks);
+      constexpr int TB = attn_tall_blocks<HD>();
+      const uint32_t lds_tall = (uint32_t)(2 * TB * sizeof(AttnBlock<HD>));
       if (best_nw == 6)
-        UAD_LAUNCH((attn_kernel<HD, 1, true, 6>), g2, dim3(384), lds, s, ev0, end_attn, at);
+        UAD_LAUNCH((attn_kernel<HD, TB, true, 6>), g2, dim3(384), lds_tall, s, ev0, end_attn, at);
       else if (best_nw == 7)
-        UAD_LAUNCH((attn_kernel<HD, 1, true, 7>), g2, dim3(448), lds, s, ev0, end_attn, at);
+        UAD_LAUNCH((attn_kernel<HD, TB, true, 7>), g2, dim3(448), lds_tall, s, ev0, end_attn, at);
       else
-        UAD_LAUNCH((attn_kernel<HD, 1, true, 8>), g2, dim3(512), lds, s, ev0, end_attn, at);
+        UAD_LAUNCH((attn_kernel<HD, TB, true, 8>), g2, dim3(512), lds_tall, s, ev0, end_attn, at);
       return hipGetLastError();
     }
   }
@@ -456,15 +467,18 @@ static hipError_t init_hd() {
   if (e == hipSuccess)
     e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 4>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             streamed_lds);
+  constexpr int TB = attn_tall_blocks<HD>();
+  constexpr int tall_lds = (int)(2 * TB * sizeof(AttnBlock<HD>));
+  static_assert(tall_lds <= 160 * 1024, "stages exceed the LDS of a CU");
   if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 6>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            streamed_lds);
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, TB, true, 6>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            tall_lds);
   if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 7>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            streamed_lds);
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, TB, true, 7>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            tall_lds);
   if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void *)attn_kernel<HD, 1, true, 8>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            streamed_lds);
+    e = hipFuncSetAttribute((const void *)attn_kernel<HD, TB, true, 8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            tall_lds);
   return e;
 }
 
