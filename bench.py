@@ -123,7 +123,7 @@ def summarize_counters(run_dir: str) -> dict:
         prev = None
         for r in rows:
             k = r["Kernel_Name"]
-            if "stamp_kernel" in k or "uad::" not in k:
+            if "stamp_kernel" in k or ("uad::" not in k and "_ZN3uad" not in k):
                 continue
             if "temb" in k:
                 cls = "temb"
@@ -179,7 +179,7 @@ def summarize_mfma(run_dir: str) -> dict:
     launches = collections.defaultdict(set)
     for r in rows:
         k = r["Kernel_Name"]
-        if "uad::" not in k or "stamp_kernel" in k:
+        if ("uad::" not in k and "_ZN3uad" not in k) or "stamp_kernel" in k:
             continue
         launches[k].add(r["Dispatch_Id"])
         per[k][r["Counter_Name"]] += float(r["Counter_Value"])
@@ -205,6 +205,48 @@ def summarize_mfma(run_dir: str) -> dict:
             "mfma_gflop_per_launch": round(512 * (c.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) +
                                                   c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)) /
                                            max(1, len(launches[k])) / 1e9, 3),
+        }
+    return out
+
+
+def summarize_lds(run_dir: str) -> dict:
+    """LDS, VALU and MFMA activity per kernel from one rocprofv3 --pmc run (SQ_LDS_IDX_ACTIVE,
+    SQ_LDS_BANK_CONFLICT, SQ_LDS_DATA_FIFO_FULL, SQ_VALU_MFMA_BUSY_CYCLES, SQ_ACTIVE_INST_VALU,
+    SQ_ACTIVE_INST_LDS, SQ_WAIT_INST_LDS, SQ_WAVE_CYCLES, GRBM_GUI_ACTIVE) found in DIR/pmc_lds:
+    the LDS counters per CU cycle (GPU active cycles of one XCC x CUs), MFMA busy per SIMD cycle,
+    the instruction-state counters per wave cycle."""
+    import csv
+    import collections
+    rows = list(csv.DictReader(open(os.path.join(run_dir, "pmc_lds", "run_counter_collection.csv"))))
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    launches = collections.defaultdict(set)
+    for r in rows:
+        k = r["Kernel_Name"]
+        if ("uad::" not in k and "_ZN3uad" not in k) or "stamp_kernel" in k:
+            continue
+        launches[k].add(r["Dispatch_Id"])
+        per[k][r["Counter_Name"]] += float(r["Counter_Value"])
+    cus, simds, xcc = 256, 1024, 8
+    agent = os.path.join(run_dir, "pmc_lds", "run_agent_info.csv")
+    if os.path.exists(agent):
+        for r in csv.DictReader(open(agent)):
+            if r.get("Agent_Type") == "GPU" and int(r.get("Simd_Count", 0) or 0) > 0:
+                simds = int(r["Simd_Count"])
+                cus = int(r.get("Cu_Count", 0) or 0) or simds // 4
+                xcc = int(r.get("Num_Xcc", 0) or 0) or xcc
+    out = {"cus": cus, "simds": simds, "xcc": xcc, "kernels": {}}
+    for k, c in per.items():
+        gui = (c.get("GRBM_GUI_ACTIVE", 0.0) / xcc) or 1.0
+        wave = c.get("SQ_WAVE_CYCLES", 0.0) or 1.0
+        out["kernels"][k] = {
+            "launches": len(launches[k]),
+            "lds_active": round(c.get("SQ_LDS_IDX_ACTIVE", 0.0) / (gui * cus), 4),
+            "lds_bank_conflict": round(c.get("SQ_LDS_BANK_CONFLICT", 0.0) / (gui * cus), 4),
+            "lds_data_fifo_full": round(c.get("SQ_LDS_DATA_FIFO_FULL", 0.0) / (gui * cus), 4),
+            "mfma_busy": round(c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui * simds), 4),
+            "valu_active": round(c.get("SQ_ACTIVE_INST_VALU", 0.0) / wave, 4),
+            "lds_inst_active": round(c.get("SQ_ACTIVE_INST_LDS", 0.0) / wave, 4),
+            "wait_lds": round(c.get("SQ_WAIT_INST_LDS", 0.0) / wave, 4),
         }
     return out
 
@@ -580,6 +622,9 @@ def main():
     ap.add_argument("--summarize-mfma", metavar="DIR", default=None,
                     help="print MFMA busy and wave-state fractions per kernel of a rocprofv3 --pmc run found in "
                          "DIR/pmc_mfma and exit; no GPU needed")
+    ap.add_argument("--summarize-lds", metavar="DIR", default=None,
+                    help="print LDS, VALU and MFMA activity per kernel of a rocprofv3 --pmc run found in "
+                         "DIR/pmc_lds and exit; no GPU needed")
     ap.add_argument("--summarize-timeline", metavar="DIR", default=None,
                     help="print the per-layer timeline of the replayed step graphs in a rocprofv3 --kernel-trace "
                          "run found in DIR (run_kernel_trace.csv) and exit; no GPU needed")
@@ -592,6 +637,9 @@ def main():
         return
     if a.summarize_mfma:
         print(json.dumps(summarize_mfma(a.summarize_mfma), indent=1))
+        return
+    if a.summarize_lds:
+        print(json.dumps(summarize_lds(a.summarize_lds), indent=1))
         return
     if a.summarize_timeline:
         print(json.dumps(summarize_timeline(a.summarize_timeline, a.workload), indent=1))
