@@ -145,6 +145,41 @@ def test_tall_query_blocks_sampled_envs(gpu):
     np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
 
 
+@pytest.mark.parametrize("name,kw,envs", [
+    # head dim 64: 128 + 211 = 339 keys, 11 key blocks, the last holding 19
+    ("tiny", dict(batch=40, chunk=128, prefix=211), (0, 39)),
+    # head dim 128: 128 + 980 = 1108 keys, 35 key blocks, the last holding 20
+    ("large_b16", dict(prefix=980), (0, 15)),
+], ids=["hd64", "hd128"])
+def test_tall_query_blocks_odd_ragged_keys(gpu, name, kw, envs):
+    """Tall attention workgroups (no split-KV) stage two key blocks at a time at
+    head dims 64 and 128; an odd block count leaves a last stage of one block,
+    and a ragged key count a partly masked last block.  Step-0 velocities of
+    sampled environments, and the first one's released actions, against the
+    oracle run alone; release steps bit-exact."""
+    c = case(name, **kw)
+    B, H = c.budgets.shape
+    assert (c.wl.prefix + c.wl.chunk) % 32 and ((c.wl.prefix + c.wl.chunk + 31) // 32) % 2 == 1
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    xg = dev(c.noise.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)), dev(mask[0].astype(np.uint8)), vg)
+    torch.cuda.synchronize()
+    v = vg.cpu().numpy()
+    _, x, rel, rst = schedule_gpu(c, c.budgets)
+    for i, b in enumerate(envs):
+        mb = c.oracle_model([b])
+        e = rel_err(v[b], O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0])
+        log(f"[{name} P={c.wl.prefix} H={H}] env {b}: step-0 velocity rel err {e:.2e}")
+        assert e <= VEL_RTOL
+        if i == 0:
+            r = O.denoise_schedule(mb, c.noise[b:b + 1], c.budgets[b:b + 1])
+            ea = float(np.abs(rel[b] - r["released"][0]).max())
+            log(f"[{name} P={c.wl.prefix} H={H}] env {b}: released abs err {ea:.2e}")
+            assert ea <= ACT_ATOL
+    np.testing.assert_array_equal(rst, O.release_steps(c.budgets))
+
+
 def test_fp16_operand_overflow_raises_range_status(gpu):
     """An activation beyond the fp16 range (the fp32 action input projection
     scaled by 1e7, so that |W_in x| is far above 65504 in the time MLP's fp16
