@@ -235,3 +235,38 @@ def test_split_partials_sized_for_every_prefix(gpu):
             assert e <= VEL_RTOL
     finally:
         ex.close()
+
+
+def _random_shapes(seed, n):
+    """n seeded (batch, chunk, prefix) triples of the small model: 1..24 environments,
+    1..128 actions, 0..700 prefix tokens (crossing the split-KV, tall-workgroup and
+    ragged-block boundaries of the attention and the small-M / batched projections)."""
+    rs = np.random.RandomState(seed)
+    return [(int(rs.randint(1, 25)), int(rs.randint(1, 129)), int(rs.randint(0, 701))) for _ in range(n)]
+
+
+@pytest.mark.parametrize("B,H,P", _random_shapes(20261202, 8))
+def test_random_shapes_every_env(gpu, B, H, P):
+    """Seeded random shapes of the small model, every environment against the
+    oracle: step-0 velocities, then a whole schedule's released actions, final
+    states and release steps."""
+    c = make_case("tiny", batch=B, chunk=H, prefix=P)
+    try:
+        m = c.oracle_model()
+        n, t, dt, mask = O.build_schedule(c.budgets)
+        xg = dev(c.noise.astype(np.float32))
+        vg = torch.empty_like(xg)
+        c.expert.step(xg, dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)),
+                      dev(mask[0].astype(np.uint8)), vg)
+        torch.cuda.synchronize()
+        v_ref = O.velocity(m, c.noise, t[0])
+        ev = max(rel_err(vg.cpu().numpy()[b], v_ref[b]) for b in range(B))
+        r = O.denoise_schedule(m, c.noise, c.budgets)
+        _, x, rel, rst = schedule_gpu(c, c.budgets)
+        ea = float(np.abs(rel - r["released"]).max())
+        ex = float(np.abs(x - r["x"]).max())
+        log(f"[tiny B={B} H={H} P={P}] worst step-0 velocity rel err {ev:.2e}, released {ea:.2e}, final {ex:.2e}")
+        assert ev <= VEL_RTOL and ea <= ACT_ATOL and ex <= ACT_ATOL
+        np.testing.assert_array_equal(rst, r["release_step"])
+    finally:
+        c.expert.close()
