@@ -467,6 +467,12 @@ def measure(ex, wl, budgets, noise, steps_req, warmup_req, sched_reps, U, np, to
     prof = U.uad_profile_read(ex.ctx)
     U.uad_profile_enable(ex.ctx, False)
     kb, kf = kernel_bytes(wl, M), kernel_flops(wl, M)
+    if getattr(s, "conditioning", "input") == "adarms" and M <= 256:
+        # schedule-level conditioning: the time MLP and the modulation GEMM run
+        # once per schedule over the rows of all its n steps
+        kbn, kfn = kernel_bytes(wl, M * n), kernel_flops(wl, M * n)
+        for c in ("gemm_mod", "gemm_time_in", "gemm_time_out"):
+            kb[c], kf[c] = kbn[c], kfn[c]
     per_kernel = {}
     for name, (ms, cnt) in prof.items():
         if cnt == 0:
@@ -574,6 +580,39 @@ def batched_leg(name, a, U, W, np, torch):
             "data": "synthetic, drawn on the device (seeded torch generator, same distributions)"}
 
 
+def adarms_leg(name, a, U, W, np, torch):
+    """The adaptive-norm expert (pi0.5-scale, batch 1) measured in the same run:
+    ms per joint step, steps per second, whole-step HBM fraction over its
+    weight bytes (+36% for the modulation matrices) and the dominant kernel
+    class against HBM peak."""
+    wl = W.get_workload(name)
+    s = wl.shape
+    t0 = time.time()
+    weights, k, v, noise = device_inputs(wl, U, W, np, torch)
+    ex = U.ActionExpert(s, wl.batch, wl.chunk, wl.prefix)
+    ex.load_weights(weights)
+    ex.set_prefix_kv(k, v, wl.batch, wl.prefix)
+    del weights, k, v
+    torch.cuda.synchronize()
+    log(f"[bench] {name}: set-up {time.time() - t0:.1f} s (inputs drawn on the device)")
+    budgets = W.make_budgets(wl)
+    meas = measure(ex, wl, budgets, noise, a.steps, a.warmup, min(a.sched_reps, 20), U, np, torch)
+    ex.close()
+    torch.cuda.empty_cache()
+    ms = meas["ms_per_step"]
+    sb = step_bytes(wl)
+    return {"config": {"workload": name, "batch": wl.batch, "chunk": wl.chunk, "prefix": wl.prefix,
+                       "layers": s.n_layers, "width": s.d_model,
+                       "heads": f"{s.n_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.d_ff,
+                       "conditioning": "adaptive RMSNorm (per-token time modulates every norm and gates every branch)",
+                       "schedule": f"{wl.budget_kind} {meas['n']} steps"},
+            "ms_per_step": round(ms, 5), "steps_per_s": round(1e3 / ms, 2),
+            "steps": meas["steps"], "warmup": meas["warmup"],
+            "bytes_per_step": sb, "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "roofline": meas["roofline"], "kernels": meas["kernels"], "schedule_time": meas["schedule_time"],
+            "data": "synthetic, drawn on the device (seeded torch generator, same distributions)"}
+
+
 def time_budget_schedules(ex, wl, budgets, noise, reps, np, torch):
     """Device time of whole schedules run from budgets (finished environments
     skipped), median and 95% bootstrap interval over reps schedules."""
@@ -613,7 +652,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-aal", action="store_true")
     ap.add_argument("--no-batched", action="store_true",
-                    help="skip the batched (MFMA-bound) legs: 64-environment fleet and the large expert")
+                    help="skip the extra legs: 64-environment fleet, the large expert and the adaptive-norm expert")
     ap.add_argument("--sched-reps", type=int, default=100,
                     help="schedules timed one by one for the median / bootstrap interval (fewer for profiler runs)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
@@ -712,6 +751,7 @@ def main():
         out["batched"] = {}
         for name in ("pi0_fleet_b64", "large_b16"):
             out["batched"][name] = batched_leg(name, a, U, W, np, torch)
+        out["adarms"] = adarms_leg("pi05_b1_adarms", a, U, W, np, torch)
 
     if not a.no_cpu_baseline:
         log("[bench] timing the oracle on the host cores")
