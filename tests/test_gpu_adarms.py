@@ -162,3 +162,29 @@ def test_adarms_schedule_level_conditioning_step_counts(gpu, top):
     e = rel_err(vg.cpu().numpy(), O.velocity(c.oracle_model(), c.noise, t))
     log(f"[tiny_adarms] single step after the schedule: velocity rel err {e:.2e}")
     assert e <= VEL_RTOL
+
+
+@pytest.mark.parametrize("pattern", ["16_times", "50_times"])
+def test_adarms_many_flow_times_one_step(gpu, pattern):
+    """A joint step of the pi0.5-scale adaptive-norm expert after a schedule
+    (schedule-level conditioning in place) whose 50 tokens take 16 flow times
+    in an irregular order, or 50 distinct ones: every token's norms get their
+    own modulations; against the oracle."""
+    c = case("pi05_b1_adarms")
+    H = c.wl.chunk
+    n, tg, dtg, mg = c.expert.schedule_tables(np.full((1, H), 10, np.int32))
+    xs = dev(c.noise.astype(np.float32))
+    c.expert.schedule(xs, tg, dtg, mg)
+    if pattern == "16_times":
+        t = (((np.arange(H) * 7) % 16 + 1) / np.float32(17)).astype(np.float32)[None]
+        assert len(np.unique(t)) == 16
+    else:
+        t = np.linspace(0.95, 0.05, H, dtype=np.float32)[None]
+        assert len(np.unique(t)) == H
+    xg = dev(c.noise.astype(np.float32))
+    vg = torch.empty_like(xg)
+    c.expert.step(xg, dev(t), dev(np.zeros_like(t)), dev(np.zeros(t.shape, np.uint8)), vg)
+    torch.cuda.synchronize()
+    e = rel_err(vg.cpu().numpy(), O.velocity(c.oracle_model(), c.noise, t))
+    log(f"[pi05_b1_adarms {pattern}] velocity rel err {e:.2e}")
+    assert e <= VEL_RTOL
