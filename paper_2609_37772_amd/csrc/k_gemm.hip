@@ -914,10 +914,33 @@ static bool resid_prefers_96(const GemmArgs &g) {
   return g.N % 96 == 0 && per_cu(6) < per_cu(8);
 }
 
+template <int EPI, int CT>
+static bool big_khalves(const GemmArgs &g);
+
+// Below MinM rows the ring still wins for QKV where the register-streamed
+// kernel would not take its k-halves (K < 1536), and for the residual
+// projections once the ring's tiles fill half the CUs.  Same-box A/B on the
+// 1024-wide expert (ms per joint step): 24 environments 2.803 -> 2.733, 32
+// 3.326 -> 3.262, 40 3.548 -> 3.321, 48 3.964 -> 3.780; QKV at 2000 rows
+// 33.4 -> 26.4 us, down 50.6 -> 46.6 us; unchanged at 80-104 residual tiles
+// (the k-halves win there) and on the 1536-wide expert.
+template <int EPI>
+static bool ring_rows_ok(const GemmArgs &g) {
+  using S = RingShape<EPI>;
+  if (g.M >= S::MinM) return true;
+  if (g.M < 1024) return false;
+  if constexpr (EPI == EPI_QKV) return !big_khalves<EPI_QKV, 8>(g);
+  if constexpr (EPI == EPI_RESID_F32) {
+    const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
+    return 2 * tiles >= g_n_cu;
+  }
+  return false;
+}
+
 template <int EPI>
 static bool ring_fits(const GemmArgs &g) {
   using S = RingShape<EPI>;
-  return g.M >= S::MinM && g.N % (16 * S::CT) == 0 && g.A2 == nullptr && g.K / kTileK >= 1 &&
+  return ring_rows_ok<EPI>(g) && g.N % (16 * S::CT) == 0 && g.A2 == nullptr && g.K / kTileK >= 1 &&
          !(EPI == EPI_QKV && g.q_dim % 16 != 0) && !(EPI == EPI_RESID_F32 && resid_prefers_96(g));
 }
 
