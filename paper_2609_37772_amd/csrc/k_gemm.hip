@@ -918,22 +918,22 @@ template <int EPI, int CT>
 static bool big_khalves(const GemmArgs &g);
 
 // Below MinM rows the ring still wins for QKV where the register-streamed
-// kernel would not take its k-halves (K < 1536), and for the residual
-// projections once the ring's tiles fill half the CUs.  Same-box A/B on the
-// 1024-wide expert (ms per joint step): 24 environments 2.803 -> 2.733, 32
-// 3.326 -> 3.262, 40 3.548 -> 3.321, 48 3.964 -> 3.780; QKV at 2000 rows
-// 33.4 -> 26.4 us, down 50.6 -> 46.6 us; unchanged at 80-104 residual tiles
-// (the k-halves win there) and on the 1536-wide expert.
+// kernel would not take its k-halves (K < 1536) once its tiles reach 3/8 of
+// the CUs, and for the residual projections once they fill half the CUs.
+// Same-box A/B on the 1024-wide expert (ms per joint step): 20 environments
+// 2.451 -> 2.364, 15 2.079 -> 2.054, 24 2.803 -> 2.733, 32 3.326 -> 3.262, 40 3.548 -> 3.321, 48
+// 3.964 -> 3.780; QKV at 750 / 1000 / 2000 rows 21.4 / 25.0 / 33.4 -> 19.5 /
+// 20.2 / 26.4 us, down at 2000 rows 50.6 -> 46.6 us. The ring lost for QKV
+// at 60-80 tiles (300-500 rows), for the residual projections at 80-104
+// tiles (the k-halves win there), for gate/up below 1024 rows, and on the
+// 1536-wide expert.
 template <int EPI>
 static bool ring_rows_ok(const GemmArgs &g) {
   using S = RingShape<EPI>;
   if (g.M >= S::MinM) return true;
-  if (g.M < 1024) return false;
-  if constexpr (EPI == EPI_QKV) return !big_khalves<EPI_QKV, 8>(g);
-  if constexpr (EPI == EPI_RESID_F32) {
-    const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
-    return 2 * tiles >= g_n_cu;
-  }
+  const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
+  if constexpr (EPI == EPI_QKV) return 8 * tiles >= 3 * g_n_cu && !big_khalves<EPI_QKV, 8>(g);
+  if constexpr (EPI == EPI_RESID_F32) return 2 * tiles >= g_n_cu;
   return false;
 }
 
