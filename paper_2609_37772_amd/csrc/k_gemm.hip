@@ -920,9 +920,10 @@ static bool big_khalves(const GemmArgs &g);
 // Below MinM rows the ring still wins for QKV where the register-streamed
 // kernel would not take its k-halves (K < 1536) once its tiles reach 3/8 of
 // the CUs, and for the residual projections once they fill half the CUs.
-// Same-box A/B on the 1024-wide expert (ms per joint step): 20 environments
-// 2.451 -> 2.364, 15 2.079 -> 2.054, 24 2.803 -> 2.733, 32 3.326 -> 3.262, 40 3.548 -> 3.321, 48
-// 3.964 -> 3.780; QKV at 750 / 1000 / 2000 rows 21.4 / 25.0 / 33.4 -> 19.5 /
+// Same-box A/B on the 1024-wide expert (ms per joint step): 15 environments
+// 2.079 -> 2.054, 20 2.451 -> 2.364, 24 2.803 -> 2.733, 32 3.326 -> 3.262,
+// 40 3.548 -> 3.321, 48 3.964 -> 3.780; QKV at 750 / 1000 / 2000 rows
+// 21.4 / 25.0 / 33.4 -> 19.5 /
 // 20.2 / 26.4 us, down at 2000 rows 50.6 -> 46.6 us. The ring lost for QKV
 // at 60-80 tiles (300-500 rows), for the residual projections at 80-104
 // tiles (the k-halves win there), for gate/up below 1024 rows, and on the
