@@ -47,6 +47,22 @@ MUTANTS = [
     ("vanilla step sign", "dtk = -(np.float32(1) / np.float32(N))", "dtk = np.float32(1) / np.float32(N)"),
     ("adaptive norm scale without 1 +", "return r * (h.dtype.type(1) + scale) + shift", "return r * scale + shift"),
     ("adaptive norm gate dropped", 'h = h + ga * (g @ W[p + "w_down"].T)', 'h = h + (g @ W[p + "w_down"].T)'),
+    ("GeGLU gate and up swapped", 'g = gelu_tanh(n2 @ W[p + "w_gate"].T) * (n2 @ W[p + "w_up"].T)',
+     'g = gelu_tanh(n2 @ W[p + "w_up"].T) * (n2 @ W[p + "w_gate"].T)'),
+    ("chunk keys and values dropped",
+     "k_all = np.concatenate([m.prefix_k[env][l], k], axis=0)\n        v_all = np.concatenate([m.prefix_v[env][l], v], axis=0)",
+     "k_all = m.prefix_k[env][l]\n        v_all = m.prefix_v[env][l]"),
+    ("time MLP SiLU dropped", 'z = silu(u @ W["time_mlp_in.w"].T + W["time_mlp_in.b"])',
+     'z = u @ W["time_mlp_in.w"].T + W["time_mlp_in.b"]'),
+    ("time frequencies without the 1000 factor", "(1000.0 * np.power(10000.0, -j / (d // 2)))",
+     "(np.power(10000.0, -j / (d // 2)))"),
+    ("adaptive norm shift dropped", "return r * (h.dtype.type(1) + scale) + shift", "return r * (h.dtype.type(1) + scale)"),
+    ("GAC dimension mask ignored", "shift = np.where(np.asarray(dim_mask, bool)[None, :], shift, 0)", "shift = shift"),
+    ("adaptive conditioning outer SiLU dropped",
+     'c = silu(silu(e @ W["time_mlp_in.w"].T + W["time_mlp_in.b"]) @ W["time_mlp_out.w"].T + W["time_mlp_out.b"])',
+     'c = silu(e @ W["time_mlp_in.w"].T + W["time_mlp_in.b"]) @ W["time_mlp_out.w"].T + W["time_mlp_out.b"]'),
+    ("final norm takes a layer's gain", 'nf = rms_norm(h, W["final_norm"], m.rms_eps)',
+     'nf = rms_norm(h, W["layers.0.mlp_norm"], m.rms_eps)'),
 ]
 
 
