@@ -94,7 +94,7 @@ def kernel_source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_37772_amd", "csrc", "*"))):
-        if f.endswith((".hip", ".cpp", ".h")):
+        if f.endswith((".hip", ".inl", ".cpp", ".h")):
             h.update(os.path.basename(f).encode())
             with open(f, "rb") as fh:
                 h.update(fh.read())

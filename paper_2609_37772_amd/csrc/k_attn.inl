@@ -108,7 +108,9 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
     return;
   }
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  // the batched variants take the wave index through readfirstlane (scalar
+  // per-wave addressing; 64 environments 39.7 -> 39.0 us)
+  const int wave = LOWREG ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) : threadIdx.x >> 6;
   // XCD-aware placement: the query blocks of one (environment-head, split)
   // group read the same K/V tiles, so the group's workgroups get ids on one
   // XCD (workgroup i runs on XCD i % 8) and share its L2; groups are dealt

@@ -641,7 +641,8 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
   __shared__ float rstd_s[128];
   int mt0, nt0;
   if (!big_tile<CT>(g, mt0, nt0)) return;  // whole workgroup: padding of the grid
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // wave index through readfirstlane: scalar per-wave addressing, up to 14 fewer VGPRs
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wq = wave & 3, kh = wave >> 2;  // position in the 2 x 2 wave grid, k-half
   const int wr = wq & 1, wc = wq >> 1;
   const int KB = g.K / kTileK;
@@ -794,7 +795,13 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
 // Residual projections on the QKV shape (with epilogue, same-box A/B against
 // the 8-wave k-halves of the register-streamed kernel): 3200 x 1024 x 2048
 // 31.1 -> 29.0 us, x 4096 52.6 -> 48.9 us (2 x 4 waves; 4 x 2: 29.9 / 50.7);
-// the 1536-wide expert's (2048 rows, 96-column tiles there) lose 5%.
+// the 1536-wide expert's (2048 rows, 96-column tiles there) lose 5% on
+// 128 x 128 ring tiles (192 tiles for 256 CUs) but win on 128 x 96 ones
+// (256 tiles, 4 x 2 waves of 32 x 48, 14 fragment blocks per stage): down
+// 64.7 -> 62.9 us, O 22.4 -> 21.6 us.
+// The wave index goes through readfirstlane so that the compiler keeps the
+// per-wave addressing and branches in scalar registers: gate/up on the
+// 1536-wide expert 82.1 -> 79.6 us.
 constexpr int kRingNW = 8;
 template <int EPI>
 struct RingShape;
@@ -811,14 +818,32 @@ struct RingShape<EPI_RESID_F32> {
   static constexpr int RT = 8, CT = 8, WR = 2, WC = 4, NS = 4, MinM = 2560;
 };
 
-template <int EPI, int NS = RingShape<EPI>::NS>
+// 128 x 96 tiles: the residual projections where 96-column tiles are preferred
+struct RingResid96 {
+  static constexpr int RT = 8, CT = 6, WR = 4, WC = 2, NS = 4, MinM = 1024;
+};
+
+// Wait until this wave's loads of all but the newest `later` stages (L
+// LDS-direct loads each) have landed, then meet the workgroup.
+template <int L>
+__device__ __forceinline__ void ring_wait(int later) {
+  if (later >= 2)
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * L) : "memory");
+  else if (later == 1)
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(L) : "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int EPI, int NS = RingShape<EPI>::NS, class S = RingShape<EPI>>
 __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
-  using S = RingShape<EPI>;
   constexpr int RT = S::RT, CT = S::CT, WR = S::WR, WC = S::WC;
-  constexpr int NBLK = RT + CT, LPW = NBLK / kRingNW;  // LDS-direct loads per wave per stage
+  // NBLK fragment blocks per stage over the 8 waves: the first NFULL waves
+  // issue LPW LDS-direct loads per stage, the others LPW - 1
+  constexpr int NBLK = RT + CT, LPW = (NBLK + kRingNW - 1) / kRingNW, NFULL = NBLK - (LPW - 1) * kRingNW;
   constexpr int TA = RT / WR, TB = CT / WC;            // 16 x 16 tiles per wave
   constexpr int ROWS = 16 * RT, TPR = 512 / ROWS;       // rows per workgroup, threads per row's statistics
-  static_assert(WR * WC == kRingNW && NBLK % kRingNW == 0, "ring shape");
+  static_assert(WR * WC == kRingNW && RT % WR == 0 && CT % WC == 0 && NS >= 2 && NS <= 4, "ring shape");
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ __align__(16) unsigned char ring_smem[];
   op_t *stage = (op_t *)ring_smem;  // [NS][NBLK][512]
@@ -827,7 +852,7 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   int pm, pn;
   if (!grid_tile(g.M, ROWS, g.N / (16 * CT), pm, pn)) return;  // whole workgroup
   const int mt0 = pm * RT, nt0 = pn * CT;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wr = wave % WR, wc = wave / WR;
   const int KB = g.K / kTileK;
   const int mt_last = g.m_alloc / 16 - 1;
@@ -837,6 +862,7 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
 #pragma unroll
     for (int q = 0; q < LPW; ++q) {
       const int bidx = wave + q * kRingNW;
+      if (NFULL < kRingNW && q == LPW - 1 && wave >= NFULL) break;
       const op_t *src = bidx < RT ? g.A + ((size_t)min(mt0 + bidx, mt_last) * KB + kb) * kBlockElems
                                   : g.W + ((size_t)(nt0 + bidx - RT) * KB + kb) * kBlockElems;
       __builtin_amdgcn_global_load_lds((const void *)(src + lane * 8), (lds_void *)(dst + bidx * kBlockElems), 16, 0,
@@ -866,12 +892,10 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
     // stage kb landed for this wave (later stages may stay in flight), then
     // for every wave; the buffer refilled below was last read one step ago
     const int later = min(NS - 2, KB - 1 - kb);  // stages issued after kb
-    if (later >= 2)
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPW) : "memory");
-    else if (later == 1)
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPW) : "memory");
+    if (NFULL == kRingNW || wave < NFULL)
+      ring_wait<LPW>(later);
     else
-      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      ring_wait<LPW - 1>(later);
     if (kb + NS - 1 < KB) issue(kb + NS - 1, (kb + NS - 1) % NS);
     const op_t *sb = stage + (size_t)(kb % NS) * NBLK * kBlockElems + lane * 8;
     f16x8 af[TA], bf[TB];
@@ -945,12 +969,23 @@ static bool ring_fits(const GemmArgs &g) {
          !(EPI == EPI_QKV && g.q_dim % 16 != 0) && !(EPI == EPI_RESID_F32 && resid_prefers_96(g));
 }
 
-template <int EPI, int NS>
+// The residual projections where 96-column tiles are preferred, on the
+// 128 x 96 ring from 1024 rows once its tiles fill 3/4 of the CUs, or with
+// a long K.  1536-wide expert, same-box (us): at 2048 and 1536 rows O 22.4 /
+// 21.8 -> 21.8 / 21.1, down 65.2 / 64.8 -> 63.7 / 62.4; at 1024 rows (128
+// tiles) down (K = 6144) 60.1 -> 58.1 but O (K = 1536) 18.0 -> 19.6, where
+// the register-streamed kernel's k-halves keep the short K ahead.
+static bool ring96_fits(const GemmArgs &g) {
+  const int tiles = (g.M + 16 * RingResid96::RT - 1) / (16 * RingResid96::RT) * (g.N / (16 * RingResid96::CT));
+  return g.M >= RingResid96::MinM && (4 * tiles >= 3 * g_n_cu || g.K >= 4096) && resid_prefers_96(g) &&
+         g.A2 == nullptr && g.K / kTileK >= 1;
+}
+
+template <int EPI, int NS, class S = RingShape<EPI>>
 static hipError_t launch_ring_ns(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  using S = RingShape<EPI>;
   const int wgs = grid_tile_wgs(g.M, 16 * S::RT, g.N / (16 * S::CT));
   const uint32_t lds = (uint32_t)(NS * (S::RT + S::CT) * kBlockElems * sizeof(op_t));
-  UAD_LAUNCH((gemm_ring_kernel<EPI, NS>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
+  UAD_LAUNCH((gemm_ring_kernel<EPI, NS, S>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
 
@@ -964,10 +999,9 @@ static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, 
   return launch_ring_ns<EPI, RingShape<EPI>::NS>(g, s, ev0, ev1);
 }
 
-template <int EPI, int NS>
+template <int EPI, int NS, class S = RingShape<EPI>>
 static hipError_t ring_attr_ns() {
-  using S = RingShape<EPI>;
-  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI, NS, S>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              NS * (S::RT + S::CT) * kBlockElems * (int)sizeof(op_t));
 }
 
@@ -1083,6 +1117,7 @@ hipError_t gemm_init() {
   if (e == hipSuccess) e = ring_attr<EPI_GEGLU>();
   if (e == hipSuccess) e = ring_attr<EPI_QKV>();
   if (e == hipSuccess) e = ring_attr<EPI_RESID_F32>();
+  if (e == hipSuccess) e = ring_attr_ns<EPI_RESID_F32, RingResid96::NS, RingResid96>();
   if (e == hipSuccess) e = big_attr<EPI_BIAS_SILU>();
   if (e == hipSuccess) e = big_attr<EPI_RESID_F32>();
   if (e == hipSuccess) e = big_attr<EPI_GEGLU>();
@@ -1135,6 +1170,8 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
   if (g.m_alloc < g.M || g.m_alloc % 16 != 0) return hipErrorInvalidValue;  // operand rows allocated
   if (epi == EPI_GEGLU && ring_fits<EPI_GEGLU>(g)) return launch_ring<EPI_GEGLU>(g, s, ev0, ev1);
   if (epi == EPI_QKV && ring_fits<EPI_QKV>(g)) return launch_ring<EPI_QKV>(g, s, ev0, ev1);
+  if (epi == EPI_RESID_F32 && ring96_fits(g))
+    return launch_ring_ns<EPI_RESID_F32, RingResid96::NS, RingResid96>(g, s, ev0, ev1);
   if (epi == EPI_RESID_F32 && ring_fits<EPI_RESID_F32>(g)) return launch_ring<EPI_RESID_F32>(g, s, ev0, ev1);
   if (big_ok(epi, g)) {
     switch (epi) {

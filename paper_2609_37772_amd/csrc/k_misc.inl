@@ -118,13 +118,14 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
     }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      if (r >= rows) break;  // uniform over the workgroup
-      const int m = m0 + r;
-      h[(size_t)m * d + n] = acc[r];
-      float sq = acc[r] * acc[r];
-      sq = sum_row16(sq);
-      if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
-      if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]), bad);
+      if (r < rows) {  // uniform over the workgroup
+        const int m = m0 + r;
+        h[(size_t)m * d + n] = acc[r];
+        float sq = acc[r] * acc[r];
+        sq = sum_row16(sq);
+        if ((n & 15) == 0) ssq[(size_t)(n >> 4) * m_alloc + m] = sq;
+        if (mod_a0) store_op(next + afrag_index(m, n, KB), acc[r] * (1.0f + mod_a0[(size_t)m * mod_ld + n]), bad);
+      }
     }
   }
   const int half = d >> 1;
