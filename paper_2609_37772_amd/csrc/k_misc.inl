@@ -40,6 +40,30 @@ __device__ __forceinline__ int load_action_rows(const float *__restrict__ x, int
   return rows;
 }
 
+// acc[r] += sum_j xs[r][j] w[j] over one W_in row (this thread's output
+// column), in j order.  16-byte loads when the row allows: each of a wave's
+// load instructions then touches every lane's 128-byte row once, where
+// 4-byte loads touched 64 rows per instruction 32 times over.
+template <int R>
+__device__ __forceinline__ void action_row_dot(const float *__restrict__ w, int Da, const float (*xs)[64],
+                                               float (&acc)[R]) {
+  if ((Da & 3) == 0 && ((uintptr_t)w & 15) == 0) {
+    for (int j = 0; j < Da; j += 4) {
+      const f32x4 w4 = *(const f32x4 *)(w + j);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] += xs[r][j + e] * w4[e];  // rows past the end: never stored
+    }
+  } else {
+    for (int j = 0; j < Da; ++j) {
+      const float wj = w[j];
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] += xs[r][j] * wj;
+    }
+  }
+}
+
 // te[m] = [ x_m W_in^T + b_in ; sin(w t_m) ; cos(w t_m) ] as the fp16 operand
 // of the time MLP in fragment order (K = 2d): the per-token flow-time
 // conditioning placed before the action MLP.  Workgroup (g, y): tokens
@@ -62,12 +86,7 @@ __global__ __launch_bounds__(256) void temb_kernel(const float *__restrict__ x, 
     const float bn = b_in[n];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = bn;
-    const float *w = w_in + (size_t)n * Da;
-    for (int j = 0; j < Da; ++j) {
-      const float wj = w[j];
-#pragma unroll
-      for (int r = 0; r < R; ++r) acc[r] += xs[r][j] * wj;  // rows past the end: never stored
-    }
+    action_row_dot<R>(w_in + (size_t)n * Da, Da, xs, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r)
       if (r < rows) store_op(te + afrag_index(m0 + r, n, KB), acc[r], bad);
@@ -110,12 +129,7 @@ __global__ __launch_bounds__(256) void temb_ada_kernel(const float *__restrict__
     const float bn = b_in[n];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = bn;
-    const float *w = w_in + (size_t)n * Da;
-    for (int j = 0; j < Da; ++j) {
-      const float wj = w[j];
-#pragma unroll
-      for (int r = 0; r < R; ++r) acc[r] += xs[r][j] * wj;
-    }
+    action_row_dot<R>(w_in + (size_t)n * Da, Da, xs, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       if (r < rows) {  // uniform over the workgroup
