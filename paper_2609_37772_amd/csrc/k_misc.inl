@@ -235,59 +235,75 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs f) {
   if (threadIdx.x < kFinalOuts && a0 + threadIdx.x < f.Da) euler_out(f, m, a0 + threadIdx.x, vs[threadIdx.x]);
 }
 
-// Batched steps (many tokens, no adaptive norm, no debug field): R tokens per
-// workgroup share every W_out load (one W_out read per R tokens; one token
-// per workgroup read W_out 3200 times per step at 64 environments).
-template <int NC, int R>
-__global__ __launch_bounds__(256) void final_rows_kernel(FinalArgs f) {
-  __shared__ float red[4][R];
-  __shared__ float wsum[4][R][kFinalOuts];
-  const int m0 = blockIdx.x * R;
-  const int a0 = blockIdx.y * kFinalOuts;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int d = f.d;
-  float gv[NC], wv[kFinalOuts][NC], hv[R][NC];
+// Batched steps (many tokens, no adaptive norm, no debug field): the
+// projection as a product on the fp32 MFMA (v_mfma_f32_16x16x4_f32), 16
+// tokens x all Da outputs per workgroup, the d columns split over its 4
+// waves: v = rstd * ((h * gain) W_out^T) + b_out.  The row-blocked form it
+// replaces spent its time in 72 wave reductions per wave (one per token and
+// output) and re-read h once per group of 8 outputs.  Within a wave, k-step
+// (q, e) of lane group kq = lane / 16 covers column c0 + 16 q + 4 kq + e, so
+// each lane reads 16-byte runs of h, gain and W_out and feeds the same
+// column to both operands.  The k-groups run in batches of 8 (uniform trip
+// count: the loop bound does not depend on kq), loads first.
+template <int NT>
+__global__ __launch_bounds__(256) void final_mfma_kernel(FinalArgs f) {
+  __shared__ f32x4 part[4][NT][64];  // per wave and output tile: each lane's accumulators
+  __shared__ float ssq[4][64];       // per wave and lane: partial sum of squares of the lane's row
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m0 = blockIdx.x * 16, kq = lane >> 4;
+  const float *__restrict__ hr = f.h + (size_t)min(m0 + (lane & 15), f.M - 1) * f.d;  // rows past M: never stored
+  const float *__restrict__ wr[NT];
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const bool in = threadIdx.x + 256 * i < d;  // clamped duplicate columns contribute nothing
-    const int c = min(threadIdx.x + 256 * i, d - 1);
-    const float g = f.gain[c];
-    gv[i] = in ? g : 0.f;
+  for (int t = 0; t < NT; ++t) wr[t] = f.w_out + (size_t)min(16 * t + (lane & 15), f.Da - 1) * f.d;
+  const int cpw = f.d >> 2;  // columns per wave (d % 512 == 0: whole batches)
+  f32x4 acc[NT];
 #pragma unroll
-    for (int o = 0; o < kFinalOuts; ++o) wv[o][i] = f.w_out[(size_t)min(a0 + o, f.Da - 1) * d + c];
+  for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float ss = 0.f;
+  // batches of 8 k-groups of 16 columns: all their loads go out before the first MFMA
+  for (int b = 0; b < cpw; b += 128) {
+    const int cb = wave * cpw + 4 * kq + b;
+    f32x4 hv[8], gv[8], wv[8][NT];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const float hh = f.h[(size_t)min(m0 + r, f.M - 1) * d + c];
-      hv[r][i] = in ? hh : 0.f;
+    for (int u = 0; u < 8; ++u) {
+      hv[u] = *(const f32x4 *)(hr + cb + 16 * u);
+      gv[u] = *(const f32x4 *)(f.gain + cb + 16 * u);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) wv[u][t] = *(const f32x4 *)(wr[t] + cb + 16 * u);
     }
+    __builtin_amdgcn_sched_barrier(0);  // keep the batch's loads ahead of its MFMAs
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ss += hv[u][e] * hv[u][e];
+        const float a = hv[u][e] * gv[u][e];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wv[u][t][e], acc[t], 0, 0, 0);
+      }
   }
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    float ss = 0.f;
-#pragma unroll
-    for (int i = 0; i < NC; ++i) ss += hv[r][i] * hv[r][i];
-    ss = sum_wave64(ss);
-    if (lane == 0) red[wave][r] = ss;
-  }
+  for (int t = 0; t < NT; ++t) part[wave][t][lane] = acc[t];
+  ssq[wave][lane] = ss;
   __syncthreads();
+  // thread (i, j): token m0 + i, outputs 16 t + j; D[i][j] of a tile sits in
+  // lane j + 16 (i / 4), component i % 4
+  const int i = threadIdx.x >> 4, j = threadIdx.x & 15, m = m0 + i;
+  if (m >= f.M) return;
+  float s2 = 0.f;
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const float rstd = 1.0f / sqrtf(((red[0][r] + red[1][r]) + (red[2][r] + red[3][r])) / (float)d + f.eps);
+  for (int w = 0; w < 4; ++w)
 #pragma unroll
-    for (int o = 0; o < kFinalOuts; ++o) {
-      float acc = 0.f;
+    for (int q = 0; q < 4; ++q) s2 += ssq[w][i + 16 * q];
+  const float rstd = 1.0f / sqrtf(s2 / (float)f.d + f.eps);
+  const int src = j + 16 * (i >> 2), cmp = i & 3;
 #pragma unroll
-      for (int i = 0; i < NC; ++i) acc += (hv[r][i] * rstd * gv[i]) * wv[o][i];
-      acc = sum_wave64(acc);
-      if (lane == 0) wsum[wave][r][o] = acc;
+  for (int t = 0; t < NT; ++t) {
+    const int a = 16 * t + j;
+    if (a < f.Da) {
+      const float v = (part[0][t][src][cmp] + part[1][t][src][cmp]) + (part[2][t][src][cmp] + part[3][t][src][cmp]);
+      euler_out(f, m, a, rstd * v + f.b_out[a]);
     }
-  }
-  __syncthreads();
-  if (threadIdx.x < R * kFinalOuts) {
-    const int r = threadIdx.x / kFinalOuts, o = threadIdx.x - r * kFinalOuts;
-    const int m = m0 + r, a = a0 + o;
-    if (m < f.M && a < f.Da)
-      euler_out(f, m, a, ((wsum[0][r][o] + wsum[1][r][o]) + (wsum[2][r][o] + wsum[3][r][o])) + f.b_out[a]);
   }
 }
 
@@ -405,14 +421,13 @@ hipError_t launch_time_features(const float *t, int M, int m_alloc, int n_steps,
 }
 
 hipError_t launch_final(const FinalArgs &f, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  if (f.M >= 1024 && !f.debug_field && !f.mod_scale) {
-    constexpr int R = 8;
-    const dim3 gr((f.M + R - 1) / R, (f.Da + kFinalOuts - 1) / kFinalOuts);
-    switch ((f.d + 255) / 256) {
-      case 4: UAD_LAUNCH((final_rows_kernel<4, R>), gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
-      case 6: UAD_LAUNCH((final_rows_kernel<6, R>), gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
-      case 8: UAD_LAUNCH((final_rows_kernel<8, R>), gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
-      default: break;  // other widths: one token per workgroup
+  if (f.M >= 1024 && !f.debug_field && !f.mod_scale && f.d % 512 == 0 && f.Da <= 64) {
+    const dim3 gr((f.M + 15) / 16);
+    switch ((f.Da + 15) / 16) {
+      case 1: UAD_LAUNCH(final_mfma_kernel<1>, gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
+      case 2: UAD_LAUNCH(final_mfma_kernel<2>, gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
+      case 3: UAD_LAUNCH(final_mfma_kernel<3>, gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
+      case 4: UAD_LAUNCH(final_mfma_kernel<4>, gr, dim3(256), 0, s, ev0, ev1, f); return hipGetLastError();
     }
   }
   const dim3 grid(f.M, (f.Da + kFinalOuts - 1) / kFinalOuts);
