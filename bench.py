@@ -254,12 +254,16 @@ def summarize_lds(run_dir: str) -> dict:
 STEP_ROLES = ("qkv", "attention", "combine", "o", "gateup", "down")
 
 
+MAX_GAPS_US = 25.0  # summed gaps between a step's kernels for the step to count as traced back to back
+
+
 def summarize_timeline(run_dir: str, workload: str = "pi0_b1") -> dict:
     """Per-layer timeline of the replayed step graphs of a rocprofv3 --kernel-trace run
     (DIR/run_kernel_trace.csv). A step is the run of kernels from the time embedding to the
-    final Euler kernel: 3 + 6 per layer + 1. Only steps whose kernels ran back to back (gaps
-    summing to under 2 us) are kept: the profiler stretches the others. For each position:
-    mean duration, mean gap before it, and the time its algorithmic bytes need at HBM peak."""
+    final Euler kernel: 3 + 6 per layer + 1. Only steps whose kernels ran nearly back to back
+    (gaps summing to under MAX_GAPS_US, a few percent of the step) are kept: the profiler
+    stretches the others. For each position: mean duration, mean gap before it, and the time
+    its algorithmic bytes need at HBM peak."""
     import csv
     import statistics
     import uad_workloads as W
@@ -284,7 +288,7 @@ def summarize_timeline(run_dir: str, workload: str = "pi0_b1") -> dict:
             if len(cur) == len(want) and all(w in n for w, (n, _, _) in zip(want, cur)):
                 steps.append(cur)
             cur = None
-    tight = [s for s in steps if sum(max(0, s[i][1] - s[i - 1][2]) for i in range(1, len(s))) < 2000]
+    tight = [s for s in steps if sum(max(0, s[i][1] - s[i - 1][2]) for i in range(1, len(s))) < MAX_GAPS_US * 1e3]
     if not tight:
         raise SystemExit("no back-to-back steps in the trace")
     dur = [statistics.mean((s[i][2] - s[i][1]) / 1e3 for s in tight) for i in range(len(want))]
@@ -302,6 +306,8 @@ def summarize_timeline(run_dir: str, workload: str = "pi0_b1") -> dict:
     return {
         "workload": workload, "steps_in_trace": len(steps), "back_to_back_steps": len(tight),
         "step_span_us": round(statistics.mean((s[-1][2] - s[0][1]) / 1e3 for s in tight), 2),
+        "step_busy_us": round(statistics.mean(sum((k[2] - k[1]) / 1e3 for k in s) for s in tight), 2),
+        "max_gaps_us": MAX_GAPS_US,
         "prologue_us": {"temb": round(dur[0], 2), "time_in": round(dur[1], 2), "time_out": round(dur[2], 2)},
         "final_us": round(dur[-1], 2),
         "gaps_total_us": round(sum(gap), 2),

@@ -42,11 +42,12 @@ def _step_kernels(layers):
 
 
 def test_summarize_timeline_keeps_back_to_back_steps(tmp_path):
-    """Two traced steps of the 18-layer batch-1 step: one back to back (each
-    kernel 1000 ns + 100 ns per position), one with 5 us gaps (dropped)."""
+    """Three traced steps of the 18-layer batch-1 step (each kernel 1000 ns + 100 ns
+    per position): one back to back, one with 100 ns gaps (11.1 us in all: kept), one
+    with 5 us gaps (dropped)."""
     names = _step_kernels(W.get_workload("pi0_b1").shape.n_layers)
     rows, t = [], 1_000_000
-    for gap in (0, 5000):
+    for gap in (0, 100, 5000):
         for i, n in enumerate(names):
             d = 1000 + 100 * (i % 7)
             rows.append([n, t, t + d])
@@ -55,13 +56,14 @@ def test_summarize_timeline_keeps_back_to_back_steps(tmp_path):
     rows.append(["uad::stamp_kernel(unsigned long*)", t, t + 500])
     _write_csv(str(tmp_path / "run_kernel_trace.csv"), ["Kernel_Name", "Start_Timestamp", "End_Timestamp"], rows)
     s = bench.summarize_timeline(str(tmp_path), "pi0_b1")
-    assert s["steps_in_trace"] == 2 and s["back_to_back_steps"] == 1
-    assert s["gaps_total_us"] == 0.0 and len(s["layers"]) == 18
+    assert s["steps_in_trace"] == 3 and s["back_to_back_steps"] == 2
+    assert s["gaps_total_us"] == pytest.approx(0.05 * (len(names) - 1)) and len(s["layers"]) == 18
     # layer 0 starts at position 3: durations 1000 + 100 * ((3 + j) % 7) ns
     assert s["layers"][0]["kernels_us"] == {r: (1000 + 100 * ((3 + j) % 7)) / 1e3
                                             for j, r in enumerate(bench.STEP_ROLES)}
-    span = sum(1000 + 100 * (i % 7) for i in range(len(names)))
-    assert s["step_span_us"] == pytest.approx(span / 1e3)
+    busy = sum(1000 + 100 * (i % 7) for i in range(len(names))) / 1e3
+    assert s["step_busy_us"] == pytest.approx(busy)
+    assert s["step_span_us"] == pytest.approx(busy + 0.05 * (len(names) - 1))
 
 
 def test_summarize_lds_and_mfma_normalisation(tmp_path):
