@@ -395,10 +395,10 @@ __host__ __device__ __forceinline__ int grid_tile_wgs(int M, int rows, int tn) {
   return ((M + rows - 1) / rows * tn + 7) / 8 * 8;
 }
 
-__device__ __forceinline__ bool grid_tile(int M, int rows, int tn, int &pm, int &pn) {
+__device__ __forceinline__ bool grid_tile_at(int wg, int M, int rows, int tn, int &pm, int &pn) {
   const int tm = (M + rows - 1) / rows, T = tm * tn;
   const int per = (T + 7) / 8;
-  const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  const int t = (wg & 7) * per + (wg >> 3);
   if (t >= T) return false;
   constexpr int GM = 8;
   const int grp = t / (GM * tn), in = t - grp * GM * tn;
@@ -406,6 +406,10 @@ __device__ __forceinline__ bool grid_tile(int M, int rows, int tn, int &pm, int 
   pm = gm0 + in % gms;
   pn = in / gms;
   return true;
+}
+
+__device__ __forceinline__ bool grid_tile(int M, int rows, int tn, int &pm, int &pn) {
+  return grid_tile_at((int)blockIdx.x, M, rows, tn, pm, pn);
 }
 
 template <int CT>
@@ -835,8 +839,9 @@ __device__ __forceinline__ void ring_wait(int later) {
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int EPI, int NS = RingShape<EPI>::NS, class S = RingShape<EPI>>
+template <int EPI, int NS = RingShape<EPI>::NS, class S = RingShape<EPI>, bool KSPLIT = false>
 __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
+  static_assert(!KSPLIT || EPI == EPI_RESID_F32, "split-K: residual projections");
   constexpr int RT = S::RT, CT = S::CT, WR = S::WR, WC = S::WC;
   // NBLK fragment blocks per stage over the 8 waves: the first NFULL waves
   // issue LPW LDS-direct loads per stage, the others LPW - 1
@@ -849,12 +854,18 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   op_t *stage = (op_t *)ring_smem;  // [NS][NBLK][512]
   __shared__ float rpart[TPR][ROWS];
   __shared__ float rstd_s[ROWS];
+  // split-K: the grid is kx copies of the tile grid, copy `split` taking the
+  // split-th of kx equal k-ranges
+  const int kx = KSPLIT ? g.kx : 1;
+  const int tn = g.N / (16 * CT), per_split = grid_tile_wgs(g.M, ROWS, tn);
+  const int split = KSPLIT ? (int)blockIdx.x / per_split : 0;
   int pm, pn;
-  if (!grid_tile(g.M, ROWS, g.N / (16 * CT), pm, pn)) return;  // whole workgroup
+  if (!grid_tile_at((int)blockIdx.x - split * per_split, g.M, ROWS, tn, pm, pn)) return;  // whole workgroup
   const int mt0 = pm * RT, nt0 = pn * CT;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wr = wave % WR, wc = wave / WR;
-  const int KB = g.K / kTileK;
+  const int KBt = g.K / kTileK;  // k-blocks of a row
+  const int kb0 = split * KBt / kx, KB = (split + 1) * KBt / kx - kb0;  // this workgroup's k-blocks
   const int mt_last = g.m_alloc / 16 - 1;
 
   auto issue = [&](int kb, int buf) {
@@ -863,8 +874,8 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
     for (int q = 0; q < LPW; ++q) {
       const int bidx = wave + q * kRingNW;
       if (NFULL < kRingNW && q == LPW - 1 && wave >= NFULL) break;
-      const op_t *src = bidx < RT ? g.A + ((size_t)min(mt0 + bidx, mt_last) * KB + kb) * kBlockElems
-                                  : g.W + ((size_t)(nt0 + bidx - RT) * KB + kb) * kBlockElems;
+      const op_t *src = bidx < RT ? g.A + ((size_t)min(mt0 + bidx, mt_last) * KBt + kb0 + kb) * kBlockElems
+                                  : g.W + ((size_t)(nt0 + bidx - RT) * KBt + kb0 + kb) * kBlockElems;
       __builtin_amdgcn_global_load_lds((const void *)(src + lane * 8), (lds_void *)(dst + bidx * kBlockElems), 16, 0,
                                        0);
     }
@@ -907,6 +918,55 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
     for (int i = 0; i < TA; ++i)
 #pragma unroll
       for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(bf[j], af[i], acc[i][j], 0, 0, 0);
+  }
+
+  if constexpr (KSPLIT) {
+    // Partial tiles, fp32, [tile][split][wave][i][j][component][lane]: the
+    // last workgroup of a tile to arrive adds them in split order, whatever
+    // the arrival order, and runs the epilogue; the others are done, and no
+    // workgroup waits on another.  The partials are written and read with
+    // device-coherent (agent-scope) stores and loads, which bypass the
+    // per-XCD L2, so no cache-wide write-back or invalidation is needed: the
+    // stores are complete (vmcnt) before the workgroup's arrival is counted.
+    __shared__ unsigned kx_last;
+    constexpr int PW = TA * TB * 4 * 64;  // floats per wave
+    const int tile = pm * tn + pn;
+    float *ws = g.kx_ws + (size_t)tile * kx * kRingNW * PW + (size_t)wave * PW + lane;
+#pragma unroll
+    for (int i = 0; i < TA; ++i)
+#pragma unroll
+      for (int j = 0; j < TB; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          __hip_atomic_store(ws + (size_t)split * kRingNW * PW + ((i * TB + j) * 4 + c) * 64, acc[i][j][c],
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0)
+      kx_last = __hip_atomic_fetch_add(g.kx_cnt + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                (unsigned)(kx - 1);
+    __syncthreads();
+    if (!kx_last) return;
+    f32x4 own[TA][TB];
+#pragma unroll
+    for (int i = 0; i < TA; ++i)
+#pragma unroll
+      for (int j = 0; j < TB; ++j) own[i][j] = acc[i][j];
+    for (int sp = 0; sp < kx; ++sp) {
+      const float *src = ws + (size_t)sp * kRingNW * PW;
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) {
+          f32x4 v = own[i][j];
+          if (sp != split)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              v[c] = __hip_atomic_load(src + ((i * TB + j) * 4 + c) * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          acc[i][j] = sp == 0 ? v : acc[i][j] + v;
+        }
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(g.kx_cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
   if (g.use_rstd) {
@@ -981,11 +1041,34 @@ static bool ring96_fits(const GemmArgs &g) {
          g.A2 == nullptr && g.K / kTileK >= 1;
 }
 
-template <int EPI, int NS, class S = RingShape<EPI>>
+// Split-K of the batched residual projections on the ring: kx = CUs / tiles
+// (at most 4) copies of the tile grid, each over an equal k-range of at least
+// 16 k-blocks, when the tiles fill at most half the CUs and are at least the
+// 90 the batched kernels need (64 with K >= 4096); 1 (no split) otherwise, or
+// when the context gave no workspace or it is too small.  Same-box A/B, ms
+// per joint step: 1024-wide expert at 32 environments (1600 rows, 104 tiles)
+// 3.130 -> 2.663 (down 49.8 -> 29.1 us, O 25.3 -> 20.4 us), 1536-wide expert
+// at 8 environments (1024 rows, 128 tiles of 96 columns) 4.450 -> 3.893
+// (down 58.0 -> 36.3 us); below 90 tiles the small-M kernel kept O and the
+// time MLP ahead (1000 rows: O 16.8 -> 18.0 us split four ways) while down
+// still won (28.1 -> 23.4 us), and at 400-600 rows both lost.
+template <class S>
+static int resid_ksplit(const GemmArgs &g) {
+  if (!g.kx_ws || !g.kx_cnt || g.A2 || g.M < kBigM || g.N % (16 * S::CT) != 0) return 1;
+  const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
+  if (tiles < 90 && !(g.K >= 4096 && tiles >= 64)) return 1;
+  int kx = std::min(4, g_n_cu / std::max(tiles, 1));
+  while (kx > 1 && (g.K / kTileK) / kx < 16) --kx;
+  constexpr size_t part = (size_t)kRingNW * (S::RT / S::WR) * (S::CT / S::WC) * 4 * 64 * sizeof(float);
+  if (kx > 1 && ((size_t)tiles * kx * part > g.kx_ws_bytes || tiles > g.kx_tiles)) return 1;
+  return kx;
+}
+
+template <int EPI, int NS, class S = RingShape<EPI>, bool KSPLIT = false>
 static hipError_t launch_ring_ns(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  const int wgs = grid_tile_wgs(g.M, 16 * S::RT, g.N / (16 * S::CT));
+  const int wgs = grid_tile_wgs(g.M, 16 * S::RT, g.N / (16 * S::CT)) * (KSPLIT ? g.kx : 1);
   const uint32_t lds = (uint32_t)(NS * (S::RT + S::CT) * kBlockElems * sizeof(op_t));
-  UAD_LAUNCH((gemm_ring_kernel<EPI, NS, S>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
+  UAD_LAUNCH((gemm_ring_kernel<EPI, NS, S, KSPLIT>), dim3(wgs), dim3(512), lds, s, ev0, ev1, g);
   return hipGetLastError();
 }
 
@@ -999,9 +1082,9 @@ static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, 
   return launch_ring_ns<EPI, RingShape<EPI>::NS>(g, s, ev0, ev1);
 }
 
-template <int EPI, int NS, class S = RingShape<EPI>>
+template <int EPI, int NS, class S = RingShape<EPI>, bool KSPLIT = false>
 static hipError_t ring_attr_ns() {
-  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI, NS, S>, hipFuncAttributeMaxDynamicSharedMemorySize,
+  return hipFuncSetAttribute((const void *)gemm_ring_kernel<EPI, NS, S, KSPLIT>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              NS * (S::RT + S::CT) * kBlockElems * (int)sizeof(op_t));
 }
 
@@ -1118,6 +1201,8 @@ hipError_t gemm_init() {
   if (e == hipSuccess) e = ring_attr<EPI_QKV>();
   if (e == hipSuccess) e = ring_attr<EPI_RESID_F32>();
   if (e == hipSuccess) e = ring_attr_ns<EPI_RESID_F32, RingResid96::NS, RingResid96>();
+  if (e == hipSuccess) e = ring_attr_ns<EPI_RESID_F32, RingShape<EPI_RESID_F32>::NS, RingShape<EPI_RESID_F32>, true>();
+  if (e == hipSuccess) e = ring_attr_ns<EPI_RESID_F32, RingResid96::NS, RingResid96, true>();
   if (e == hipSuccess) e = big_attr<EPI_BIAS_SILU>();
   if (e == hipSuccess) e = big_attr<EPI_RESID_F32>();
   if (e == hipSuccess) e = big_attr<EPI_GEGLU>();
@@ -1170,6 +1255,17 @@ hipError_t launch_gemm(int epi, const GemmArgs &g, const GemmPlan &p, hipStream_
   if (g.m_alloc < g.M || g.m_alloc % 16 != 0) return hipErrorInvalidValue;  // operand rows allocated
   if (epi == EPI_GEGLU && ring_fits<EPI_GEGLU>(g)) return launch_ring<EPI_GEGLU>(g, s, ev0, ev1);
   if (epi == EPI_QKV && ring_fits<EPI_QKV>(g)) return launch_ring<EPI_QKV>(g, s, ev0, ev1);
+  if (epi == EPI_RESID_F32) {
+    GemmArgs gk = g;
+    if (resid_prefers_96(g)) {
+      gk.kx = resid_ksplit<RingResid96>(g);
+      if (gk.kx > 1) return launch_ring_ns<EPI_RESID_F32, RingResid96::NS, RingResid96, true>(gk, s, ev0, ev1);
+    } else {
+      using S8 = RingShape<EPI_RESID_F32>;
+      gk.kx = resid_ksplit<S8>(g);
+      if (gk.kx > 1) return launch_ring_ns<EPI_RESID_F32, S8::NS, S8, true>(gk, s, ev0, ev1);
+    }
+  }
   if (epi == EPI_RESID_F32 && ring96_fits(g))
     return launch_ring_ns<EPI_RESID_F32, RingResid96::NS, RingResid96>(g, s, ev0, ev1);
   if (epi == EPI_RESID_F32 && ring_fits<EPI_RESID_F32>(g)) return launch_ring<EPI_RESID_F32>(g, s, ev0, ev1);

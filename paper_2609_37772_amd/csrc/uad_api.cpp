@@ -357,7 +357,8 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
          o_mod = a.take<float>(M * c->n_mod), o_mshift = a.take<uint16_t>(c->ada ? (size_t)2 * c->L * M * d : 0),
          o_pf = a.take<unsigned>(64), o_status = a.take<unsigned>(1),
          o_budt = a.take<float>(kMaxTrSteps * M), o_buddt = a.take<float>(kMaxTrSteps * M),
-         o_budm = a.take<uint8_t>(kMaxTrSteps * M), o_budmap = a.take<int32_t>((size_t)kMaxTrSteps * m.max_batch);
+         o_budm = a.take<uint8_t>(kMaxTrSteps * M), o_budmap = a.take<int32_t>((size_t)kMaxTrSteps * m.max_batch),
+         o_kxw = a.take<float>((size_t)c->n_cu * kKxPartialFloats), o_kxc = a.take<unsigned>((size_t)c->n_cu);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -388,6 +389,9 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->bud_dt = (float *)(ab + o_buddt);
   c->bud_mask = (uint8_t *)(ab + o_budm);
   c->bud_map = (int32_t *)(ab + o_budmap);
+  c->kx_ws = (float *)(ab + o_kxw);
+  c->kx_cnt = (unsigned *)(ab + o_kxc);
+  c->kx_ws_bytes = (size_t)c->n_cu * kKxPartialFloats * sizeof(float);
   e = attention_init();
   if (e == hipSuccess) e = gemm_init();
   // the no-allocation step's scratch: its address on this device (a failure is
@@ -712,6 +716,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
     // RMSNorm folding: residual GEMMs write ssq and the next operand; consumers scale by rstd
     auto norm_fields = [&](GemmArgs &x) {
       x.ssq = c->ssq; x.ssq_tiles = d / 16; x.m_alloc = (int)MA; x.eps = c->cfg.rms_eps;
+      x.kx_ws = c->kx_ws; x.kx_cnt = c->kx_cnt; x.kx_ws_bytes = c->kx_ws_bytes; x.kx_tiles = c->n_cu;
     };
     const int n_mod = c->n_mod;
     if (!c->ada) {

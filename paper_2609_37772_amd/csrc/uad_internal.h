@@ -50,6 +50,9 @@ typedef _Float16 op_t;
 // n-tile major, so one 16-column tile's whole K stream is contiguous and each
 // lane's operand is one aligned 16-byte load.
 constexpr int kMaxTrSteps = 64;  // longest canonical schedule N* of the release path
+// fp32 elements of one split-K partial tile (a 128 x 128 output tile); the
+// context holds one per CU
+constexpr size_t kKxPartialFloats = 128 * 128;
 constexpr int kTileN = 16;
 constexpr int kTileK = 32;
 constexpr int kBlockElems = kTileN * kTileK;  // 512 fp16 = 1 KiB
@@ -195,6 +198,16 @@ struct GemmArgs {
   // compacted steps: environment j of this step is environment env_map[j] of
   // the caller's batch (its K/V store slot); null when every environment runs
   const int32_t *env_map;
+  // Split-K of the batched residual projections when their tiles leave most
+  // CUs idle (null workspace: never).  kx_ws holds the fp32 partial tiles
+  // (kx_ws_bytes), kx_cnt one arrival counter per output tile, zero between
+  // launches (the last workgroup of a tile to arrive resets it); kx is the
+  // split count of the launch, set by the launcher.
+  float *kx_ws;
+  unsigned *kx_cnt;
+  size_t kx_ws_bytes;
+  int kx_tiles;  // counters available
+  int kx;
 };
 
 // Up to two byte ranges (weights of the next projections) that otherwise idle
@@ -388,6 +401,9 @@ struct uad_ctx {
   int n_cu = 0;  // compute units of the device
   size_t attn_part_elems = 0;
   float *ssq = nullptr;   // per-tile sums of squares of h [d/16][m_alloc]
+  float *kx_ws = nullptr;     // split-K partial tiles of the batched residual projections
+  unsigned *kx_cnt = nullptr; // their per-tile arrival counters (zeroed at creation)
+  size_t kx_ws_bytes = 0;
   void *abuf = nullptr;
 
   // adaptive-norm conditioning (flag UAD_FLAG_ADARMS)
