@@ -270,3 +270,36 @@ def test_random_shapes_every_env(gpu, B, H, P):
         np.testing.assert_array_equal(rst, r["release_step"])
     finally:
         c.expert.close()
+
+
+@pytest.mark.parametrize("Da", [7, 20])
+def test_batched_final_projection_ragged_rows_and_outputs(gpu, Da):
+    """The batched final projection (fp32 MFMA from 1024 tokens when the width is a
+    multiple of 512): 21 environments x 50 actions = 1050 token rows (the last
+    16-row tile holds 10), Da = 7 (one partial output tile) or 20 (a full and a
+    partial one), width 512, every environment against the oracle: step-0
+    velocities, then a whole schedule's released actions, final states and
+    release steps."""
+    import uad_workloads as W
+    shape = W.ModelShape(2, 512, 4, 4, 64, 1024, Da)
+    c = make_case("tiny", batch=21, chunk=50, prefix=40, shape=shape)
+    try:
+        m = c.oracle_model()
+        n, t, dt, mask = O.build_schedule(c.budgets)
+        xg = dev(c.noise.astype(np.float32))
+        vg = torch.empty_like(xg)
+        c.expert.step(xg, dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)),
+                      dev(mask[0].astype(np.uint8)), vg)
+        torch.cuda.synchronize()
+        v_ref = O.velocity(m, c.noise, t[0])
+        ev = max(rel_err(vg.cpu().numpy()[b], v_ref[b]) for b in range(c.wl.batch))
+        r = O.denoise_schedule(m, c.noise, c.budgets)
+        _, x, rel, rst = schedule_gpu(c, c.budgets)
+        ea = float(np.abs(rel - r["released"]).max())
+        ex = float(np.abs(x - r["x"]).max())
+        log(f"[final rows 1050, Da={Da}, d=512] worst step-0 velocity rel err {ev:.2e}, released {ea:.2e}, "
+            f"final {ex:.2e}")
+        assert ev <= VEL_RTOL and ea <= ACT_ATOL and ex <= ACT_ATOL
+        np.testing.assert_array_equal(rst, r["release_step"])
+    finally:
+        c.expert.close()
