@@ -121,7 +121,10 @@ typedef struct {
  * null stream, so the work is ordered with everything else the caller (or
  * PyTorch's default stream) queues there.  Allocates the
  * weight store, the prefix/chunk K/V store and all activation workspace for
- * the configured maxima.  Errors: UAD_E_INVALID (null/negative fields),
+ * the configured maxima, including the split-K partial tiles of the batched
+ * residual projections (64 KiB per compute unit) and their arrival counters,
+ * which every call of the context reuses (so its calls run in stream order,
+ * never overlapping).  Errors: UAD_E_INVALID (null/negative fields),
  * UAD_E_UNSUPPORTED (dimension the kernels cannot tile), UAD_E_OOM, UAD_E_HIP.
  * On error *out is set to NULL. */
 uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_stream, uad_ctx **out);
