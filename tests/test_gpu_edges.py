@@ -311,8 +311,9 @@ def test_split_k_residual_projections(gpu, width, B, H):
     1600 rows x 1024 columns = 104 tiles of 128 x 128; 1024 rows x 1536 = 128
     tiles of 128 x 96), 2 layers of the pi0-scale and large experts' widths:
     step-0 velocities of every environment against the oracle, the same step
-    again bit for bit (the partials are added in split order whatever the
-    arrival order), then a whole schedule's released actions and final states."""
+    24 times more bit for bit (the partials are added in split order whatever
+    the arrival order), then a whole schedule's released actions and final
+    states."""
     import uad_workloads as W
     shape = (W.ModelShape(2, 1024, 8, 1, 256, 4096, 32) if width == 1024
              else W.ModelShape(2, 1536, 12, 2, 128, 6144, 32))
@@ -324,7 +325,10 @@ def test_split_k_residual_projections(gpu, width, B, H):
         args = (dev(t[0].astype(np.float32)), dev(dt[0].astype(np.float32)), dev(mask[0].astype(np.uint8)))
         v1, v2 = torch.empty_like(xg), torch.empty_like(xg)
         c.expert.step(xg.clone(), *args, v1)
-        c.expert.step(xg.clone(), *args, v2)
+        repeats_equal = True
+        for _ in range(24):  # the partials' arrival order varies from call to call; the sums must not
+            c.expert.step(xg.clone(), *args, v2)
+            repeats_equal &= bool(torch.equal(v1, v2))
         torch.cuda.synchronize()
         v_ref = O.velocity(m, c.noise, t[0])
         ev = max(rel_err(v1.cpu().numpy()[b], v_ref[b]) for b in range(B))
@@ -334,7 +338,7 @@ def test_split_k_residual_projections(gpu, width, B, H):
         ex = float(np.abs(x - r["x"]).max())
         log(f"[split-K width {width}, {B * H} rows] worst step-0 velocity rel err {ev:.2e}, released {ea:.2e}, "
             f"final {ex:.2e}")
-        assert torch.equal(v1, v2)
+        assert repeats_equal
         assert ev <= VEL_RTOL and ea <= ACT_ATOL and ex <= ACT_ATOL
         np.testing.assert_array_equal(rst, r["release_step"])
     finally:
