@@ -50,7 +50,7 @@ constexpr int attn_chunk_blocks() {
 }
 
 // Blocks per stage of the tall batched workgroups (6-8 waves): the waves
-// meet once per stage.  Same-box A/B per launch: HD = 128 (2048 tokens x 1152
+// meet once per stage.  Same-machine A/B per launch: HD = 128 (2048 tokens x 1152
 // keys) 33.2 -> 32.4 us with 2 blocks (4 blocks: 33.2); HD = 256 (3200 tokens x
 // 866 keys) 45.3 -> 46.2 us with 2, so one there.
 template <int HD>

@@ -357,7 +357,7 @@ static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, 
   }
   // Double-buffered passes hold ~200 registers, one 8-wave workgroup per CU:
   // only when the grid has no more workgroups than CUs (batch 1: down 4
-  // passes, O 2; step 0.700 -> 0.696 ms same-box; at 8 environments, 448
+  // passes, O 2; step 0.700 -> 0.696 ms same-machine; at 8 environments, 448
   // workgroups, they lost 4% against two co-resident workgroups per CU).
   if (p.passes > 1 && (long)grid.x * grid.z <= g_n_cu)
     UAD_LAUNCH((gemm_kernel<EPI, T, KPW, false, true>), grid, dim3(p.waves * 64), lds, s, ev0, ev1, g);
@@ -791,12 +791,12 @@ __global__ __launch_bounds__(256 * KS) void gemm_big_kernel(GemmArgs g) {
 //   gate/up 256 x 128, 4 x 2 waves, 3 stages: 3200 x 8192 x 1024: 800 (vs
 //   711 register-streamed), 2048 x 12288 x 1536: 960 (vs 921); with the
 //   GeGLU epilogue, 128 x 256 tiles (2 x 4 waves, same LDS per stage) beat
-//   256 x 128 in a same-box A/B: 73.3 -> 66.0 us and 89.3 -> 79.1 us (3200
+//   256 x 128 in a same-machine A/B: 73.3 -> 66.0 us and 89.3 -> 79.1 us (3200
 //   rows are 25 full 128-row panels instead of 12.5 of 256; 800 tiles
 //   instead of 832);
 //   QKV 128 x 128, 2 x 4 waves, 4 stages: 3200 x 2560 x 1024: 761 (vs 643;
 //   at 2048 x 2048 x 1536 the register-streamed kernel stays ahead, 651 vs 621).
-// Residual projections on the QKV shape (with epilogue, same-box A/B against
+// Residual projections on the QKV shape (with epilogue, same-machine A/B against
 // the 8-wave k-halves of the register-streamed kernel): 3200 x 1024 x 2048
 // 31.1 -> 29.0 us, x 4096 52.6 -> 48.9 us (2 x 4 waves; 4 x 2: 29.9 / 50.7);
 // the 1536-wide expert's (2048 rows, 96-column tiles there) lose 5% on
@@ -1004,7 +1004,7 @@ static bool big_khalves(const GemmArgs &g);
 // Below MinM rows the ring still wins for QKV where the register-streamed
 // kernel would not take its k-halves (K < 1536) once its tiles reach 3/8 of
 // the CUs, and for the residual projections once they fill half the CUs.
-// Same-box A/B on the 1024-wide expert (ms per joint step): 15 environments
+// Same-machine A/B on the 1024-wide expert (ms per joint step): 15 environments
 // 2.079 -> 2.054, 20 2.451 -> 2.364, 24 2.803 -> 2.733, 32 3.326 -> 3.262,
 // 40 3.548 -> 3.321, 48 3.964 -> 3.780; QKV at 750 / 1000 / 2000 rows
 // 21.4 / 25.0 / 33.4 -> 19.5 /
@@ -1031,7 +1031,7 @@ static bool ring_fits(const GemmArgs &g) {
 
 // The residual projections where 96-column tiles are preferred, on the
 // 128 x 96 ring from 1024 rows once its tiles fill 3/4 of the CUs, or with
-// a long K.  1536-wide expert, same-box (us): at 2048 and 1536 rows O 22.4 /
+// a long K.  1536-wide expert, same-machine (us): at 2048 and 1536 rows O 22.4 /
 // 21.8 -> 21.8 / 21.1, down 65.2 / 64.8 -> 63.7 / 62.4; at 1024 rows (128
 // tiles) down (K = 6144) 60.1 -> 58.1 but O (K = 1536) 18.0 -> 19.6, where
 // the register-streamed kernel's k-halves keep the short K ahead.
@@ -1045,7 +1045,7 @@ static bool ring96_fits(const GemmArgs &g) {
 // (at most 4) copies of the tile grid, each over an equal k-range of at least
 // 16 k-blocks, when the tiles fill at most half the CUs and are at least the
 // 90 the batched kernels need (64 with K >= 4096); 1 (no split) otherwise, or
-// when the context gave no workspace or it is too small.  Same-box A/B, ms
+// when the context gave no workspace or it is too small.  Same-machine A/B, ms
 // per joint step: 1024-wide expert at 32 environments (1600 rows, 104 tiles)
 // 3.130 -> 2.663 (down 49.8 -> 29.1 us, O 25.3 -> 20.4 us), 1536-wide expert
 // at 8 environments (1024 rows, 128 tiles of 96 columns) 4.450 -> 3.893
@@ -1073,7 +1073,7 @@ static hipError_t launch_ring_ns(const GemmArgs &g, hipStream_t s, hipEvent_t ev
 }
 
 // Gate/up with K <= 1024 on a 2-stage ring (48 KiB of LDS, three workgroups
-// per CU): same-box A/B at 3200 x 8192 x 1024 68.6 -> 65.9 us; at K = 1536
+// per CU): same-machine A/B at 3200 x 8192 x 1024 68.6 -> 65.9 us; at K = 1536
 // (2048 x 12288) the 2-stage ring lost 84.2 -> 92.6 us, so 3 stages there.
 template <int EPI>
 static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {

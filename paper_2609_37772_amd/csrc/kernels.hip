@@ -5,12 +5,12 @@
 // cache, which a pair of CUs share (64 KiB).  With the kernels in three code
 // objects the step's hot code (~53 KiB) landed at offsets that the rest of
 // the code decided: adding 8.5 KiB of unrelated batched-kernel code ahead of
-// the small-M GEMMs slowed the batch-1 step by 1.4% (same-box, identical
+// the small-M GEMMs slowed the batch-1 step by 1.4% (same-machine, identical
 // kernel code), shifting them by a further 64 KiB restored it, and the same
 // offsets with the old code reproduced the loss.  Here the kernels of that
 // step are instantiated first, in launch order, so they sit contiguously at
 // the start of the code and, being smaller than the cache, cannot evict each
-// other whatever the load address (same-box: 0.7065 -> 0.7048 ms per step,
+// other whatever the load address (same-machine: 0.7065 -> 0.7048 ms per step,
 // independent of the code that follows).
 //
 // The set is the batch-1 step of the 1024-wide expert with 256-wide heads:
