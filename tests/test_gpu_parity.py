@@ -200,8 +200,10 @@ def test_budgets_non_contiguous_finished_environments(gpu):
 
 
 def test_frozen_tokens_bit_identical_batched(gpu):
-    """Frozen tokens stay bit-identical through the 8-token-per-workgroup final
-    projection used from 1,024 token rows on (64 environments)."""
+    """Frozen tokens stay bit-identical through the batched final projection
+    (16 tokens per workgroup on MFMA, used from 1,024 token rows on when the
+    width is a multiple of 512: here 64 environments x 50 tokens, width 1024),
+    a -0.0 among them."""
     c = case("pi0_fleet_b64")
     n, tg, dtg, mg = c.expert.schedule_tables(c.budgets)
     x0 = c.noise.astype(np.float32).copy()
