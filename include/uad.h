@@ -122,7 +122,7 @@ typedef struct {
  * PyTorch's default stream) queues there.  Allocates the
  * weight store, the prefix/chunk K/V store and all activation workspace for
  * the configured maxima, including the split-K partial tiles of the batched
- * residual projections (64 KiB per compute unit) and their arrival counters,
+ * residual projections (128 KiB per compute unit) and their arrival counters,
  * which every call of the context reuses (so its calls run in stream order,
  * never overlapping).  Errors: UAD_E_INVALID (null/negative fields),
  * UAD_E_UNSUPPORTED (dimension the kernels cannot tile), UAD_E_OOM, UAD_E_HIP.

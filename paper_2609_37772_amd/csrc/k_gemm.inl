@@ -1051,13 +1051,20 @@ static bool ring96_fits(const GemmArgs &g) {
 // at 8 environments (1024 rows, 128 tiles of 96 columns) 4.450 -> 3.893
 // (down 58.0 -> 36.3 us); below 90 tiles the small-M kernel kept O and the
 // time MLP ahead (1000 rows: O 16.8 -> 18.0 us split four ways) while down
-// still won (28.1 -> 23.4 us), and at 400-600 rows both lost.
+// still won (28.1 -> 23.4 us), and at 400-600 rows both lost.  Tiles filling
+// more than half the CUs (one workgroup per CU) split two ways when K >= 4096,
+// two co-resident workgroups per CU instead of one: down of the 1536-wide
+// expert at 16 environments (256 tiles of 128 x 96) 65.5 -> 54.3 us, step
+// 5.595 -> 5.333 ms; of the 1024-wide at 64 environments (200 tiles) 45.3 ->
+// 43.4 us; with O and the time MLP (K = 1536-2048) split as well the step
+// lost (O 22.1 -> 24.3 us, 26.9 -> 30.3 us).
 template <class S>
 static int resid_ksplit(const GemmArgs &g) {
   if (!g.kx_ws || !g.kx_cnt || g.A2 || g.M < kBigM || g.N % (16 * S::CT) != 0) return 1;
   const int tiles = (g.M + 16 * S::RT - 1) / (16 * S::RT) * (g.N / (16 * S::CT));
   if (tiles < 90 && !(g.K >= 4096 && tiles >= 64)) return 1;
   int kx = std::min(4, g_n_cu / std::max(tiles, 1));
+  if (kx == 1 && tiles <= g_n_cu && g.K >= 4096) kx = 2;
   while (kx > 1 && (g.K / kTileK) / kx < 16) --kx;
   constexpr size_t part = (size_t)kRingNW * (S::RT / S::WR) * (S::CT / S::WC) * 4 * 64 * sizeof(float);
   if (kx > 1 && ((size_t)tiles * kx * part > g.kx_ws_bytes || tiles > g.kx_tiles)) return 1;

@@ -358,7 +358,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
          o_pf = a.take<unsigned>(64), o_status = a.take<unsigned>(1),
          o_budt = a.take<float>(kMaxTrSteps * M), o_buddt = a.take<float>(kMaxTrSteps * M),
          o_budm = a.take<uint8_t>(kMaxTrSteps * M), o_budmap = a.take<int32_t>((size_t)kMaxTrSteps * m.max_batch),
-         o_kxw = a.take<float>((size_t)c->n_cu * kKxPartialFloats), o_kxc = a.take<unsigned>((size_t)c->n_cu);
+         o_kxw = a.take<float>((size_t)2 * c->n_cu * kKxPartialFloats), o_kxc = a.take<unsigned>((size_t)c->n_cu);
   e = hipMalloc(&c->abuf, a.off);
   if (e == hipSuccess) e = hipMemset(c->abuf, 0, a.off);
   if (e != hipSuccess) {
@@ -391,7 +391,7 @@ uad_status uad_create(const uad_model_config *cfg, int32_t device, void *hip_str
   c->bud_map = (int32_t *)(ab + o_budmap);
   c->kx_ws = (float *)(ab + o_kxw);
   c->kx_cnt = (unsigned *)(ab + o_kxc);
-  c->kx_ws_bytes = (size_t)c->n_cu * kKxPartialFloats * sizeof(float);
+  c->kx_ws_bytes = (size_t)2 * c->n_cu * kKxPartialFloats * sizeof(float);
   e = attention_init();
   if (e == hipSuccess) e = gemm_init();
   // the no-allocation step's scratch: its address on this device (a failure is

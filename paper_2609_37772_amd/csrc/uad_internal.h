@@ -51,7 +51,7 @@ typedef _Float16 op_t;
 // lane's operand is one aligned 16-byte load.
 constexpr int kMaxTrSteps = 64;  // longest canonical schedule N* of the release path
 // fp32 elements of one split-K partial tile (a 128 x 128 output tile); the
-// context holds one per CU
+// context holds two per CU
 constexpr size_t kKxPartialFloats = 128 * 128;
 constexpr int kTileN = 16;
 constexpr int kTileK = 32;

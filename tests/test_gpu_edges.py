@@ -305,15 +305,19 @@ def test_batched_final_projection_ragged_rows_and_outputs(gpu, Da):
         c.expert.close()
 
 
-@pytest.mark.parametrize("width,B,H", [(1024, 32, 50), (1024, 22, 50), (1536, 8, 128), (1536, 8, 125)],
-                         ids=["w1024_1600rows", "w1024_1100rows_3way", "w1536_1024rows", "w1536_1000rows"])
+@pytest.mark.parametrize("width,B,H", [(1024, 32, 50), (1024, 22, 50), (1536, 8, 128), (1536, 8, 125),
+                                       (1024, 64, 50), (1536, 16, 128)],
+                         ids=["w1024_1600rows", "w1024_1100rows_3way", "w1536_1024rows", "w1536_1000rows",
+                              "w1024_3200rows_down", "w1536_2048rows_down"])
 def test_split_k_residual_projections(gpu, width, B, H):
     """Residual projections split over K (tiles filling at most half the CUs:
     1600 rows x 1024 columns = 104 tiles of 128 x 128, two ways; 1100 rows =
     72 tiles, down (K = 4096) three ways over uneven k-ranges of 42 and 43
     blocks; 1024 and 1000 rows x 1536 = 128 tiles of 128 x 96, two ways; the
-    1600-, 1100- and 1000-row cases end in a ragged row panel), 2 layers of the
-    pi0-scale and large experts' widths:
+    1600-, 1100- and 1000-row cases end in a ragged row panel), and only down
+    (K >= 4096), two ways, where the tiles fill more than half the CUs (3200
+    rows x 1024 = 200 tiles, 2048 rows x 1536 = 256 tiles of 96 columns),
+    2 layers of the pi0-scale and large experts' widths:
     step-0 velocities of every environment against the oracle, the same step
     24 times more bit for bit (the partials are added in split order whatever
     the arrival order), then a whole schedule's released actions and final
