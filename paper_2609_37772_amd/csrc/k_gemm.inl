@@ -382,7 +382,6 @@ static hipError_t launch_t(const GemmArgs &g, const GemmPlan &p, hipStream_t s, 
 // an L2 share weight and activation panels.  The epilogue runs from the
 // accumulators (no cross-wave reduction).
 // ---------------------------------------------------------------------------
-constexpr int kBigM = 256;
 constexpr int kBigRowTiles = 8;  // 128 rows per workgroup
 constexpr int kBigPD = 3;        // k-blocks in flight per wave
 

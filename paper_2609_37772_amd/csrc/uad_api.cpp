@@ -125,6 +125,10 @@ hipEvent_t pool_event(uad_ctx *c) {
   return e;
 }
 
+// CUs the attention launch has to leave free for the weight read-ahead of its
+// extra workgroups (below that the read-ahead is not issued).
+constexpr int kReadAheadMinCus = 32;
+
 int attn_splits_nb(const uad_ctx *c, int B, int H, int n_blocks, int *bps) {
   const int rows = (c->Hq / c->Hkv) * H;
   const int qblocks = (rows + 63) / 64;
@@ -133,12 +137,26 @@ int attn_splits_nb(const uad_ctx *c, int B, int H, int n_blocks, int *bps) {
   // workgroups (256 CUs): one chunk (one memory round trip) per split when
   // that fits (batch 1), else floor(256 / query blocks) splits (a few
   // environments; measured best at 4 and 8 environments), none when the query
-  // blocks alone fill the chip.
+  // blocks alone fill the chip.  Where the projections run on the batched
+  // kernels, fewer splits if the grid (its groups padded to a multiple of the
+  // 8 XCDs) would leave under kReadAheadMinCus CUs to the weight read-ahead:
+  // gate/up then streams its weights from HBM (~28.5 instead of ~22.5 us at
+  // 300-850 rows).  Same-machine, ms per joint step, 1024-wide expert: 6
+  // environments 1.616 -> 1.588 (6 -> 5 splits), 7 1.679 -> 1.608, 9 1.769 ->
+  // 1.695, 11 2.003 -> 1.924, 12 2.053 -> 1.947 (3 -> 2), 17 2.354 -> 2.276
+  // (2 -> 1); 1536-wide: 2 environments 2.683 -> 2.581, 5 3.395 -> 3.262.
+  // Below 256 rows (5 environments: 7 -> 6 splits, 1.442 -> 1.451 ms) the
+  // small-M projections gain less from the read-ahead than the attention
+  // loses.
   const int nb = attention_chunk_blocks(c->hd);
   int per = nb;
   if ((long)wgs * ((n_blocks + nb - 1) / nb) > 256) {
-    const int sp = std::max(1, 256 / wgs);
-    per = (n_blocks + sp - 1) / sp;
+    for (int sp = std::max(1, 256 / wgs);; --sp) {
+      per = (n_blocks + sp - 1) / sp;
+      const int splits = (n_blocks + per - 1) / per;
+      if (sp == 1 || B * H < kBigM || 8 * ((B * c->Hkv * splits + 7) / 8) * qblocks <= c->n_cu - kReadAheadMinCus)
+        break;
+    }
   }
   const int smax = attention_max_splits(c->hd);
   if ((n_blocks + per - 1) / per > smax) per = (n_blocks + smax - 1) / smax;
@@ -810,7 +828,7 @@ static uad_status enqueue_step(uad_ctx *c, hipStream_t s, float *x, const float 
       at.kc = kc; at.vtc = vtc;
       at.pre_attn = Prefetch{};
       at.pre_comb = Prefetch{};
-      if (spare_cus >= 32) {
+      if (spare_cus >= kReadAheadMinCus) {
         at.pre_attn.p[0] = (const char *)lp.wo;
         at.pre_attn.bytes[0] = (uint32_t)((size_t)d * c->q_dim * sizeof(op_t));
         at.pre_attn.p[1] = (const char *)lp.wgu;

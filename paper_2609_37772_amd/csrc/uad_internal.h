@@ -55,6 +55,9 @@ constexpr int kMaxTrSteps = 64;  // longest canonical schedule N* of the release
 constexpr size_t kKxPartialFloats = 128 * 128;
 constexpr int kTileN = 16;
 constexpr int kTileK = 32;
+// token rows from which the projections run on the batched (128-row tile)
+// kernels rather than the small-M weight-streaming one
+constexpr int kBigM = 256;
 constexpr int kBlockElems = kTileN * kTileK;  // 512 fp16 = 1 KiB
 
 // Device status word of a context (bits, cleared and reported by

@@ -244,6 +244,25 @@ def test_fleet_ragged_row_panels(gpu, batch):
     c.expert.close()
 
 
+@pytest.mark.parametrize("batch", [6, 12, 17])
+def test_fleet_small_batches_with_weight_read_ahead(gpu, batch):
+    """A few environments of the fleet model, where the attention's key splits
+    are chosen to leave CUs to the weight read-ahead (6, 12 and 17
+    environments: 5, 2 and 1 splits of the 28 key blocks) and the read-ahead
+    workgroups run in the attention and merge launches: the first and last
+    environment's step-0 velocities against the oracle run alone."""
+    c = make_case("pi0_fleet_b64", batch=batch)
+    n, t, dt, mask = O.build_schedule(c.budgets)
+    _, v = gpu_velocity(c, c.noise, t[0], dt[0], mask[0])
+    for b in (0, batch - 1):
+        mb = c.oracle_model([b])
+        v_ref = O.velocity(mb, c.noise[b:b + 1], t[0][b:b + 1])[0]
+        e = rel_err(v[b], v_ref)
+        log(f"[fleet B={batch}] env {b}: step-0 velocity rel err {e:.2e}")
+        assert e <= VEL_RTOL
+    c.expert.close()
+
+
 # ----------------------------------------------------------------------------
 # Invariants of the method on the GPU path
 # ----------------------------------------------------------------------------
