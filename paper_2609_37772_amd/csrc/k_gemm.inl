@@ -821,6 +821,12 @@ struct RingShape<EPI_RESID_F32> {
   static constexpr int RT = 8, CT = 8, WR = 2, WC = 4, NS = 4, MinM = 2560;
 };
 
+// 144 x 256 gate/up tiles, 1 x 8 waves of 144 x 32 (one gate/up pair each):
+// fewer tiles where 128-row ones would leave some CUs a fourth tile
+struct RingGeGlu144 {
+  static constexpr int RT = 9, CT = 16, WR = 1, WC = 8, NS = 3, MinM = 1024;
+};
+
 // 128 x 96 tiles: the residual projections where 96-column tiles are preferred
 struct RingResid96 {
   static constexpr int RT = 8, CT = 6, WR = 4, WC = 2, NS = 4, MinM = 1024;
@@ -883,7 +889,7 @@ __global__ __launch_bounds__(512) void gemm_ring_kernel(GemmArgs g) {
   for (int s = 0; s < NS - 1; ++s)
     if (s < KB) issue(s, s);
 
-  if (g.use_rstd) {
+  if (g.use_rstd && (TPR * ROWS == 512 || (int)threadIdx.x < TPR * ROWS)) {
     // per-row sums of squares: TPR threads share row (tid % ROWS), each summing a slice of its tiles
     const int row = min(mt0 * 16 + (int)(threadIdx.x % ROWS), g.M - 1), part = threadIdx.x / ROWS;
     const int t0 = part * g.ssq_tiles / TPR, t1 = (part + 1) * g.ssq_tiles / TPR;
@@ -1081,10 +1087,29 @@ static hipError_t launch_ring_ns(const GemmArgs &g, hipStream_t s, hipEvent_t ev
 // Gate/up with K <= 1024 on a 2-stage ring (48 KiB of LDS, three workgroups
 // per CU): same-machine A/B at 3200 x 8192 x 1024 68.6 -> 65.9 us; at K = 1536
 // (2048 x 12288) the 2-stage ring lost 84.2 -> 92.6 us, so 3 stages there.
+// Gate/up on 144-row tiles when that brings the tiles within one round of
+// co-resident ring workgroups (two per CU) and 128-row ones exceed it: the
+// tiles past the round ran as a second, mostly single-workgroup wave.
+// Same-machine, 1024-wide expert: 2050 rows (544 -> 480 tiles) 57.1 ->
+// 42.5 us, step 3.484 -> 3.210 ms; 2300 rows 56.5 -> 42.9 us; 1536-wide at
+// 1408 rows (528 -> 480 tiles, K = 1536) 75.8 -> 59.7 us, step 5.089 ->
+// 4.666 ms.  Where both exceed the round it lost (3200 rows, 800 -> 736
+// tiles: 67.0 -> 69.6 us).
+static bool geglu_prefers_144(const GemmArgs &g) {
+  const int tn = g.N / 256;
+  const int t128 = (g.M + 127) / 128 * tn, t144 = (g.M + 143) / 144 * tn;
+  return t128 > 2 * g_n_cu && t144 <= 2 * g_n_cu;
+}
+
 template <int EPI>
 static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  if constexpr (EPI == EPI_GEGLU)
+  if constexpr (EPI == EPI_GEGLU) {
+    if (geglu_prefers_144(g)) {
+      if (g.K <= 1024) return launch_ring_ns<EPI, 2, RingGeGlu144>(g, s, ev0, ev1);
+      return launch_ring_ns<EPI, RingGeGlu144::NS, RingGeGlu144>(g, s, ev0, ev1);
+    }
     if (g.K <= 1024) return launch_ring_ns<EPI, 2>(g, s, ev0, ev1);
+  }
   return launch_ring_ns<EPI, RingShape<EPI>::NS>(g, s, ev0, ev1);
 }
 
@@ -1097,8 +1122,11 @@ static hipError_t ring_attr_ns() {
 template <int EPI>
 static hipError_t ring_attr() {
   hipError_t e = ring_attr_ns<EPI, RingShape<EPI>::NS>();
-  if constexpr (EPI == EPI_GEGLU)
+  if constexpr (EPI == EPI_GEGLU) {
     if (e == hipSuccess) e = ring_attr_ns<EPI, 2>();
+    if (e == hipSuccess) e = ring_attr_ns<EPI, 2, RingGeGlu144>();
+    if (e == hipSuccess) e = ring_attr_ns<EPI, RingGeGlu144::NS, RingGeGlu144>();
+  }
   return e;
 }
 

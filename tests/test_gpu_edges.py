@@ -322,6 +322,19 @@ def test_split_k_residual_projections(gpu, width, B, H):
     24 times more bit for bit (the partials are added in split order whatever
     the arrival order), then a whole schedule's released actions and final
     states."""
+    _two_layer_case(width, B, H, "split-K")
+
+
+def test_gate_up_144_row_tiles_three_stages(gpu):
+    """Gate/up of the 1536-wide expert (K = 1536, the 3-stage ring) on 144-row
+    tiles: 11 environments x 128 tokens = 1408 rows make 528 tiles of 128 x 256
+    for 512 co-resident workgroups but 480 of 144 x 256, the last panel 112
+    rows; 2 layers, the same checks as the split-K cases (down splits two ways
+    here too)."""
+    _two_layer_case(1536, 11, 128, "gate/up 144-row tiles")
+
+
+def _two_layer_case(width, B, H, label):
     import uad_workloads as W
     shape = (W.ModelShape(2, 1024, 8, 1, 256, 4096, 32) if width == 1024
              else W.ModelShape(2, 1536, 12, 2, 128, 6144, 32))
@@ -344,7 +357,7 @@ def test_split_k_residual_projections(gpu, width, B, H):
         _, x, rel, rst = schedule_gpu(c, c.budgets)
         ea = float(np.abs(rel - r["released"]).max())
         ex = float(np.abs(x - r["x"]).max())
-        log(f"[split-K width {width}, {B * H} rows] worst step-0 velocity rel err {ev:.2e}, released {ea:.2e}, "
+        log(f"[{label} width {width}, {B * H} rows] worst step-0 velocity rel err {ev:.2e}, released {ea:.2e}, "
             f"final {ex:.2e}")
         assert repeats_equal
         assert ev <= VEL_RTOL and ea <= ACT_ATOL and ex <= ACT_ATOL
