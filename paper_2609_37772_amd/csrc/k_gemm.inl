@@ -826,6 +826,11 @@ struct RingShape<EPI_RESID_F32> {
 struct RingGeGlu144 {
   static constexpr int RT = 9, CT = 16, WR = 1, WC = 8, NS = 3, MinM = 1024;
 };
+// 160 x 256 gate/up tiles, 2 x 4 waves of 80 x 64 (two stages only: two
+// workgroups' three stages and row statistics exceed the 160 KiB of LDS)
+struct RingGeGlu160 {
+  static constexpr int RT = 10, CT = 16, WR = 2, WC = 4, NS = 3, MinM = 1024;
+};
 
 // 128 x 96 tiles: the residual projections where 96-column tiles are preferred
 struct RingResid96 {
@@ -1087,24 +1092,29 @@ static hipError_t launch_ring_ns(const GemmArgs &g, hipStream_t s, hipEvent_t ev
 // Gate/up with K <= 1024 on a 2-stage ring (48 KiB of LDS, three workgroups
 // per CU): same-machine A/B at 3200 x 8192 x 1024 68.6 -> 65.9 us; at K = 1536
 // (2048 x 12288) the 2-stage ring lost 84.2 -> 92.6 us, so 3 stages there.
-// Gate/up on 144-row tiles when that brings the tiles within one round of
-// co-resident ring workgroups (two per CU) and 128-row ones exceed it: the
-// tiles past the round ran as a second, mostly single-workgroup wave.
-// Same-machine, 1024-wide expert: 2050 rows (544 -> 480 tiles) 57.1 ->
-// 42.5 us, step 3.484 -> 3.210 ms; 2300 rows 56.5 -> 42.9 us; 1536-wide at
-// 1408 rows (528 -> 480 tiles, K = 1536) 75.8 -> 59.7 us, step 5.089 ->
-// 4.666 ms.  Where both exceed the round it lost (3200 rows, 800 -> 736
-// tiles: 67.0 -> 69.6 us).
-static bool geglu_prefers_144(const GemmArgs &g) {
+// Gate/up on the shortest of 128-, 144- and 160-row tiles that fits one round
+// of co-resident ring workgroups (two per CU), 128 when none does: the tiles
+// past the round ran as a second, mostly single-workgroup wave.  Same-machine,
+// 144 rows: 2050 rows (544 -> 480 tiles) 57.1 -> 42.5 us, step 3.484 -> 3.210
+// ms; 2300 rows 56.5 -> 42.9 us; 1536-wide at 1408 rows (528 -> 480 tiles,
+// K = 1536) 75.8 -> 59.7 us, step 5.089 -> 4.666 ms.  160 rows: 2400 rows
+// 56.6 -> 44.6 us, step 3.416 -> 3.203 ms; 2500 rows 56.1 -> 45.4 us;
+// 1536-wide at 1536 rows 75.4 -> 61.8 us, step 5.017 -> 4.676 ms.  Where
+// every shape exceeds the round the taller tiles lost (3200 rows, 800 -> 736
+// tiles of 144: 67.0 -> 69.6 us).
+static int geglu_tile_rows(const GemmArgs &g) {
   const int tn = g.N / 256;
-  const int t128 = (g.M + 127) / 128 * tn, t144 = (g.M + 143) / 144 * tn;
-  return t128 > 2 * g_n_cu && t144 <= 2 * g_n_cu;
+  for (int rows : {128, 144, 160})
+    if ((g.M + rows - 1) / rows * tn <= 2 * g_n_cu) return rows;
+  return 128;
 }
 
 template <int EPI>
 static hipError_t launch_ring(const GemmArgs &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if constexpr (EPI == EPI_GEGLU) {
-    if (geglu_prefers_144(g)) {
+    const int rows = geglu_tile_rows(g);
+    if (rows == 160) return launch_ring_ns<EPI, 2, RingGeGlu160>(g, s, ev0, ev1);
+    if (rows == 144) {
       if (g.K <= 1024) return launch_ring_ns<EPI, 2, RingGeGlu144>(g, s, ev0, ev1);
       return launch_ring_ns<EPI, RingGeGlu144::NS, RingGeGlu144>(g, s, ev0, ev1);
     }
@@ -1126,6 +1136,7 @@ static hipError_t ring_attr() {
     if (e == hipSuccess) e = ring_attr_ns<EPI, 2>();
     if (e == hipSuccess) e = ring_attr_ns<EPI, 2, RingGeGlu144>();
     if (e == hipSuccess) e = ring_attr_ns<EPI, RingGeGlu144::NS, RingGeGlu144>();
+    if (e == hipSuccess) e = ring_attr_ns<EPI, 2, RingGeGlu160>();
   }
   return e;
 }

@@ -325,13 +325,15 @@ def test_split_k_residual_projections(gpu, width, B, H):
     _two_layer_case(width, B, H, "split-K")
 
 
-def test_gate_up_144_row_tiles_three_stages(gpu):
-    """Gate/up of the 1536-wide expert (K = 1536, the 3-stage ring) on 144-row
-    tiles: 11 environments x 128 tokens = 1408 rows make 528 tiles of 128 x 256
-    for 512 co-resident workgroups but 480 of 144 x 256, the last panel 112
-    rows; 2 layers, the same checks as the split-K cases (down splits two ways
-    here too)."""
-    _two_layer_case(1536, 11, 128, "gate/up 144-row tiles")
+@pytest.mark.parametrize("B,rows", [(11, 144), (12, 160)], ids=["1408rows_144", "1536rows_160"])
+def test_gate_up_taller_tiles_long_k(gpu, B, rows):
+    """Gate/up of the 1536-wide expert (K = 1536) on taller tiles: 11
+    environments x 128 tokens = 1408 rows make 528 tiles of 128 x 256 for 512
+    co-resident workgroups but 480 of 144 x 256 (3-stage ring, the last panel
+    112 rows); 12 environments (1536 rows, 576 tiles) 480 of 160 x 256
+    (2-stage ring, the last panel 96 rows); 2 layers, the same checks as the
+    split-K cases (down splits two ways here too)."""
+    _two_layer_case(1536, B, 128, f"gate/up {rows}-row tiles")
 
 
 def _two_layer_case(width, B, H, label):

@@ -226,13 +226,15 @@ def test_frozen_tokens_bit_identical_batched(gpu):
     assert checked > 0
 
 
-@pytest.mark.parametrize("batch", [41, 48, 60])
+@pytest.mark.parametrize("batch", [41, 48, 49, 60])
 def test_fleet_ragged_row_panels(gpu, batch):
-    """Fleet model at 2050 / 2400 / 3000 token rows, not a multiple of the
-    batched kernels' 128-row panels: the k-halves projections (2400 rows), the
-    residual LDS ring (3000 rows) and the 128 x 256 gate/up ring end on a
-    partial panel, and at 2050 rows gate/up runs on 144-row tiles (15 panels,
-    the last 34 rows); the last environment's rows lie in the partial panel."""
+    """Fleet model at 2050 / 2400 / 2450 / 3000 token rows, not a multiple of
+    the batched kernels' 128-row panels: the k-halves projections (2400 rows),
+    the residual LDS ring (3000 rows) and the 128 x 256 gate/up ring end on a
+    partial panel; gate/up runs on 144-row tiles at 2050 rows (15 panels, the
+    last 34 rows) and on 160-row tiles at 2400 and 2450 rows (the last panel
+    of 2450 holds 50 rows); the last environment's rows lie in the partial
+    panel."""
     c = make_case("pi0_fleet_b64", batch=batch)
     n, t, dt, mask = O.build_schedule(c.budgets)
     _, v = gpu_velocity(c, c.noise, t[0], dt[0], mask[0])
