@@ -334,11 +334,12 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a) {
 // o = sum_s 2^(m_s - M) l_s o_s / sum_s 2^(m_s - M) l_s, splits in fixed order.  One wave per (16-row tile, 16-column tile): lane l
 // owns the float4 of the accumulator layout (rows 4*(l>>4)..+3, column l&15)
 // and reads the (m, l) pairs of its 4 rows itself, so all loads are issued
-// up front and the merge needs no LDS or barrier.
-template <int SMAX>
-__global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
-  const int rt = blockIdx.x;  // 16-row tile
-  const int nt = blockIdx.y;  // 16-column tile
+// up front and the merge needs no LDS or barrier.  W waves per workgroup take
+// W neighbouring column tiles.
+template <int SMAX, int W>
+__global__ __launch_bounds__(64 * W) void attn_combine_kernel(AttnArgs a, int hd) {
+  const int rt = blockIdx.x;                                               // 16-row tile
+  const int nt = blockIdx.y * W + (W > 1 ? (int)(threadIdx.x >> 6) : 0);  // 16-column tile
   const int eh = blockIdx.z;
   const int n_eh = a.n_eh;
   if (eh >= n_eh) {  // the extra slice prefetches
@@ -348,7 +349,7 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd) {
   const int b = eh / a.n_kv_heads, g = eh - b * a.n_kv_heads;
   const int splits = a.splits;
   const int ntiles = a.rows_pad / 16;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int rbase = (lane >> 4) * 4;
   unsigned bad = 0;  // fp16 range flag of this lane's stores
   f16x4 os[SMAX];
@@ -445,16 +446,22 @@ static hipError_t launch_hd(const AttnArgs &a, int batch, hipStream_t s, hipEven
   if (e != hipSuccess || a.splits == 1) return e;
   hipEvent_t none = nullptr;
   AttnArgs ac = a;
-  ac.pre_comb.wgs = a.pre_comb.wgs ? (a.rows_pad / 16) * (HD / 16) : 0;  // one extra z slice
-  const dim3 cgrid(a.rows_pad / 16, HD / 16, batch * a.n_kv_heads + (ac.pre_comb.wgs ? 1 : 0));
+  // Beyond 8 splits (one chunk each: batch 1) four waves per workgroup, a
+  // quarter of the workgroups to dispatch (the merge and its read-ahead slice
+  // are ~900 one-wave workgroups at batch 1): same-machine, three pairs,
+  // 0.7066 -> 0.7037 ms per step; at 8 environments (4 splits) one wave per
+  // workgroup stays ahead (1.663 vs 1.677 ms).
+  const int W = a.splits > 8 ? 4 : 1;
+  ac.pre_comb.wgs = a.pre_comb.wgs ? (a.rows_pad / 16) * (HD / (16 * W)) : 0;  // one extra z slice
+  const dim3 cgrid(a.rows_pad / 16, HD / (16 * W), batch * a.n_kv_heads + (ac.pre_comb.wgs ? 1 : 0));
   if (a.splits <= 4)
-    UAD_LAUNCH((attn_combine_kernel<4>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
+    UAD_LAUNCH((attn_combine_kernel<4, 1>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
   else if (a.splits <= 8)
-    UAD_LAUNCH((attn_combine_kernel<8>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
+    UAD_LAUNCH((attn_combine_kernel<8, 1>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
   else if (a.splits <= 16)
-    UAD_LAUNCH((attn_combine_kernel<16>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
+    UAD_LAUNCH((attn_combine_kernel<16, 4>), cgrid, dim3(256), 0, s, none, ev1, ac, HD);
   else if (a.splits <= 32)
-    UAD_LAUNCH((attn_combine_kernel<32>), cgrid, dim3(64), 0, s, none, ev1, ac, HD);
+    UAD_LAUNCH((attn_combine_kernel<32, 4>), cgrid, dim3(256), 0, s, none, ev1, ac, HD);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

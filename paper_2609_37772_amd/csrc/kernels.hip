@@ -31,8 +31,8 @@ template <int EPI, int T, int KPW, bool DUAL, bool PIPE>
 __global__ __launch_bounds__(512) void gemm_kernel(GemmArgs g);
 template <int HD, int NB, bool LOWREG, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(AttnArgs a);
-template <int SMAX>
-__global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int hd);
+template <int SMAX, int W>
+__global__ __launch_bounds__(64 * W) void attn_combine_kernel(AttnArgs a, int hd);
 template <int NC>
 __global__ __launch_bounds__(256) void final_kernel(FinalArgs f);
 
@@ -44,7 +44,7 @@ template __global__ void gemm_kernel<EPI_BIAS_SILU, 1, 4, false, true>(GemmArgs)
 template __global__ void gemm_kernel<EPI_RESID_F32, 1, 4, false, false>(GemmArgs);
 template __global__ void gemm_kernel<EPI_QKV, 1, 4, false, false>(GemmArgs);
 template __global__ void attn_kernel<256, 2, false, 4>(AttnArgs);
-template __global__ void attn_combine_kernel<16>(AttnArgs, int);
+template __global__ void attn_combine_kernel<16, 4>(AttnArgs, int);
 template __global__ void gemm_kernel<EPI_RESID_F32, 1, 4, false, true>(GemmArgs);
 template __global__ void gemm_kernel<EPI_GEGLU, 2, 4, false, false>(GemmArgs);
 template __global__ void final_kernel<4>(FinalArgs);
